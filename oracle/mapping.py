@@ -1,0 +1,117 @@
+"""CPU enumeration of the workgroup -> (batch, head, row-block) mappings.
+
+TEST INFRASTRUCTURE ONLY (the oracle): imported by the test suite, the smoke
+check and the benchmark's CPU-baseline leg, never by the product path.  It is
+written from the paper's definitions, shares no code with the HIP kernels, and
+is deliberately plain Python so it can be read against the paper.
+
+Setting (Sections 2.2, 3.1, 3.2, 3.3):
+  * A FlashAttention-2 forward grid has one workgroup (WG) per
+    (batch b, query head hq, query row block m); there are
+    NB = ceil(Sq / BM) row blocks per head (the listing of Fig. "head-first
+    code" computes blocks_per_head with a ceiling) and N = B * Hq * NB WGs in a
+    1-D grid.
+  * The hardware hands WG ``wid`` to die (XCD) ``wid mod NX``: chunked
+    round-robin with chunk size one (Section 2.2).  Within one XCD the k-th WG
+    it receives is ``wid = x + k * NX``.
+  * An Attention Compute Cluster (ACC, Section 3.1) is the set of WGs reading
+    the same K/V: one (batch, KV head) pair, the KV head of query head hq being
+    hq // (Hq // Hkv).
+
+The three mappings (integer ``mapping`` argument of the C ABI):
+  0  naive block-first (Section 3.2): block 0 of every head, then block 1 of
+     every head, ...; heads vary fastest, batch outermost.
+  1  naive head-first (Section 3.2): every block of head 0, then of head 1,
+     ...; blocks vary fastest, batch outermost.
+  2  swizzled head-first (Section 3.3): the head-first order is cut into NX
+     contiguous pieces and piece x is run by XCD x, in order.  WG ``wid`` is
+     the k-th WG of XCD x = wid mod NX (k = wid div NX); its rank in the
+     XCD-major listing is L = x*q + min(x, r) + k with q, r = divmod(N, NX),
+     and L is decoded in head-first order.  When N is a multiple of NX this is
+     exactly the chiplet swizzle of Fig. "wg-swizzle" (new id =
+     xcd * (N / NX) + local id); the min(x, r) term extends it to grids that are
+     not, where the first r XCDs take one WG more.  Batch is outermost
+     throughout (the readings of the garbled per-batch line of the listing and
+     of Hq < NX are recorded with the design notes).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+NAIVE_BLOCK_FIRST = 0
+NAIVE_HEAD_FIRST = 1
+SWIZZLED_HEAD_FIRST = 2
+MAPPINGS = (NAIVE_BLOCK_FIRST, NAIVE_HEAD_FIRST, SWIZZLED_HEAD_FIRST)
+
+
+def num_row_blocks(Sq: int, BM: int) -> int:
+    """NB = ceil(Sq / BM): the last block may be partial."""
+    return (Sq + BM - 1) // BM
+
+
+def grid_size(B: int, Hq: int, Sq: int, BM: int) -> int:
+    return B * Hq * num_row_blocks(Sq, BM)
+
+
+def unravel(x: int, radices) -> tuple:
+    """Mixed-radix digits of x, most significant first (last digit fastest)."""
+    digits = []
+    for r in reversed(radices):
+        digits.append(x % r)
+        x //= r
+    assert x == 0, "index out of range for the given radices"
+    return tuple(reversed(digits))
+
+
+def xcd_of(wid: int, NX: int) -> int:
+    """Hardware dispatch model: chunked round-robin with chunk size one."""
+    return wid % NX
+
+
+def swizzled_rank(wid: int, N: int, NX: int) -> int:
+    """Rank L of ``wid`` when the grid is listed XCD by XCD (XCD-major)."""
+    x = wid % NX
+    k = wid // NX
+    q, r = divmod(N, NX)
+    return x * q + min(x, r) + k
+
+
+def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int) -> tuple:
+    """(b, hq, m) that WG ``wid`` computes under ``mapping``."""
+    N = B * Hq * NB
+    if not 0 <= wid < N:
+        raise ValueError("wid out of range")
+    if mapping == NAIVE_BLOCK_FIRST:
+        b, m, hq = unravel(wid, (B, NB, Hq))
+    elif mapping == NAIVE_HEAD_FIRST:
+        b, hq, m = unravel(wid, (B, Hq, NB))
+    elif mapping == SWIZZLED_HEAD_FIRST:
+        b, hq, m = unravel(swizzled_rank(wid, N, NX), (B, Hq, NB))
+    else:
+        raise ValueError("unknown mapping %r" % (mapping,))
+    return b, hq, m
+
+
+def enumerate_mapping(mapping: int, B: int, Hq: int, Sq: int, BM: int, NX: int) -> np.ndarray:
+    """Array [N, 3] of (b, hq, m) for wid = 0 .. N-1 (pure-Python loop)."""
+    NB = num_row_blocks(Sq, BM)
+    N = B * Hq * NB
+    out = np.empty((N, 3), dtype=np.int64)
+    for wid in range(N):
+        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX)
+    return out
+
+
+def acc_id(b: int, hq: int, Hq: int, Hkv: int) -> int:
+    """Attention Compute Cluster of a WG: the (batch, KV head) it reads."""
+    return b * Hkv + hq // (Hq // Hkv)
+
+
+def xcd_acc_sequences(table: np.ndarray, Hq: int, Hkv: int, NX: int) -> list:
+    """For each XCD, the ACC ids of the WGs it receives, in dispatch order."""
+    seqs = [[] for _ in range(NX)]
+    for wid in range(table.shape[0]):
+        b, hq, _ = table[wid]
+        seqs[xcd_of(wid, NX)].append(acc_id(int(b), int(hq), Hq, Hkv))
+    return seqs

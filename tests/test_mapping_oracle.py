@@ -1,0 +1,221 @@
+"""Pins for the CPU enumeration of the WG -> (b, hq, m) mappings (CPU only).
+
+What ties the enumeration (oracle/mapping.py) to the paper:
+  * every mapping is a permutation of the grid, on many shapes including
+    ragged ones (N not a multiple of NX, Hq < NX);
+  * swizzled head-first equals the chiplet renumbering of Fig. "wg-swizzle"
+    (new id = (wid mod NX) * N/NX + wid div NX) whenever N is a multiple of NX;
+  * with one batch and Hq a multiple of NX it equals what the listing of
+    Fig. "head-first code" computes: head = (wid mod NX) * Hq/NX +
+    wid div (NX*NB) and block = (wid mod (NX*NB)) div NX;
+  * the caption example of Sections 3.2/3.3 (8 heads, 128 row blocks, 4 XCDs)
+    from tests/golden/caption_example.json;
+  * "one ACC at a time" (Section 3.3) for every shape whose ACC count is a
+    multiple of NX, including the GQA grouping of Section 3.1.
+Planted mistakes in the enumeration (monkeypatched) must fail a pin.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import mapping as mp
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "caption_example.json")
+
+SHAPES = [(B, Hq, NB, NX) for B in (1, 2, 3) for Hq in (1, 2, 3, 4, 5, 8, 12, 16)
+          for NB in (1, 2, 3, 7, 9) for NX in (1, 2, 4, 8)]
+
+
+def _table(m, mapping, B, Hq, NB, NX):
+    return np.array([m.map_wid(mapping, w, B, Hq, NB, NX) for w in range(B * Hq * NB)])
+
+
+def pin_permutation(m):
+    for (B, Hq, NB, NX) in SHAPES:
+        N = B * Hq * NB
+        for mapping in mp.MAPPINGS:
+            t = _table(m, mapping, B, Hq, NB, NX)
+            keys = (t[:, 0] * Hq + t[:, 1]) * NB + t[:, 2]
+            assert t.min() >= 0 and np.all(t[:, 0] < B) and np.all(t[:, 1] < Hq) \
+                and np.all(t[:, 2] < NB)
+            assert np.array_equal(np.sort(keys), np.arange(N)), (mapping, B, Hq, NB, NX)
+
+
+def pin_chiplet_swizzle(m):
+    """Fig. "wg-swizzle": XCD-major renumbering when NX divides N."""
+    for (B, Hq, NB, NX) in SHAPES:
+        N = B * Hq * NB
+        if N % NX:
+            continue
+        for wid in range(N):
+            renum = (wid % NX) * (N // NX) + wid // NX
+            assert m.map_wid(mp.SWIZZLED_HEAD_FIRST, wid, B, Hq, NB, NX) == \
+                m.unravel(renum, (B, Hq, NB))
+
+
+def pin_head_first_listing(m):
+    """Fig. "head-first code" for one batch and NX | Hq."""
+    for (B, Hq, NB, NX) in SHAPES:
+        if B != 1 or Hq % NX:
+            continue
+        for wid in range(Hq * NB):
+            head = (wid % NX) * (Hq // NX) + wid // (NX * NB)
+            block = (wid % (NX * NB)) // NX
+            assert m.map_wid(mp.SWIZZLED_HEAD_FIRST, wid, 1, Hq, NB, NX) == (0, head, block)
+
+
+def pin_caption_example(m):
+    g = json.load(open(GOLDEN))
+    s = g["shape"]
+    B, Hq, NB, NX = s["B"], s["Hq"], s["row_blocks"], s["NX"]
+    N = B * Hq * NB
+    c = g["claims"]
+    # naive block-first
+    t = _table(m, mp.NAIVE_BLOCK_FIRST, B, Hq, NB, NX)
+    for wid, (xcd, head, block) in enumerate(c["naive_block_first"]["first_dispatch"]):
+        assert m.xcd_of(wid, NX) == xcd and tuple(t[wid][1:]) == (head, block)
+    assert np.all(np.diff(t[:, 2]) >= 0)  # block-major: blocks never go back
+    # naive head-first: head-major order, every head on all XCDs
+    t = _table(m, mp.NAIVE_HEAD_FIRST, B, Hq, NB, NX)
+    assert np.all(np.diff(t[:, 1]) >= 0)
+    for h in range(Hq):
+        xcds = {m.xcd_of(w, NX) for w in range(N) if t[w][1] == h}
+        assert len(xcds) == c["naive_head_first"]["xcds_per_head"]
+    # swizzled head-first: one XCD per head, one ACC at a time, blocks in order
+    t = _table(m, mp.SWIZZLED_HEAD_FIRST, B, Hq, NB, NX)
+    for h in range(Hq):
+        wids = [w for w in range(N) if t[w][1] == h]
+        assert len({m.xcd_of(w, NX) for w in wids}) == c["swizzled_head_first"]["xcds_per_head"]
+        assert [t[w][2] for w in wids] == list(range(NB))
+    seqs = m.xcd_acc_sequences(t, Hq, s["Hkv"], NX)
+    for seq in seqs:
+        assert all(a <= b for a, b in zip(seq, seq[1:]))
+    # the illustration puts heads {2x, 2x+1} on XCD x
+    for x in range(NX):
+        assert sorted(set(seqs[x])) == [2 * x, 2 * x + 1]
+
+
+def pin_one_acc_at_a_time(m):
+    """Section 3.3: with NX | B*Hkv every ACC lives on one XCD, XCDs never revisit an ACC."""
+    shapes = [(1, 32, 32, 8192, 128), (1, 64, 8, 8192, 128), (8, 64, 64, 4096, 128),
+              (1, 16, 16, 131072, 128), (2, 16, 4, 1000, 128), (1, 8, 8, 300, 64)]
+    for (B, Hq, Hkv, Sq, BM) in shapes:
+        NX = 8
+        NB = m.num_row_blocks(Sq, BM)
+        t = np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX)
+                      for w in range(B * Hq * NB)])
+        seqs = m.xcd_acc_sequences(t, Hq, Hkv, NX)
+        owner = {}
+        for x, seq in enumerate(seqs):
+            assert all(a <= b for a, b in zip(seq, seq[1:]))
+            for a in seq:
+                assert owner.setdefault(a, x) == x, "ACC split across XCDs"
+
+
+def pin_gqa_groups_on_one_xcd(m):
+    """Llama-3-70B-like GQA (Hq=64, Hkv=8, 64 row blocks): group x runs on XCD x."""
+    B, Hq, Hkv, NB, NX = 1, 64, 8, 64, 8
+    for wid in range(B * Hq * NB):
+        _, hq, _ = m.map_wid(mp.SWIZZLED_HEAD_FIRST, wid, B, Hq, NB, NX)
+        assert hq // (Hq // Hkv) == m.xcd_of(wid, NX)
+
+
+def pin_ceil_blocks(m):
+    assert m.num_row_blocks(256, 128) == 2 and m.num_row_blocks(257, 128) == 3
+    assert m.num_row_blocks(1, 128) == 1 and m.grid_size(2, 3, 129, 128) == 12
+
+
+PINS = [pin_permutation, pin_chiplet_swizzle, pin_head_first_listing, pin_caption_example,
+        pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_ceil_blocks]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
+def test_pin(pin):
+    pin(mp)
+
+
+def test_enumerate_matches_map_wid():
+    t = mp.enumerate_mapping(mp.SWIZZLED_HEAD_FIRST, 2, 12, 300, 128, 8)
+    assert t.shape == (2 * 12 * 3, 3)
+    assert tuple(t[5]) == mp.map_wid(2, 5, 2, 12, 3, 8)
+
+
+def test_errors():
+    with pytest.raises(ValueError):
+        mp.map_wid(3, 0, 1, 1, 1, 8)
+    with pytest.raises(ValueError):
+        mp.map_wid(0, 4, 1, 2, 2, 8)
+
+
+# ---------------------------------------------------------------- planted mistakes
+
+
+class _Mutant:
+    """The enumeration module with one function replaced."""
+
+    def __init__(self, **overrides):
+        self.__dict__.update({k: getattr(mp, k) for k in dir(mp) if not k.startswith("__")})
+        self.__dict__.update(overrides)
+        # map_wid must see the replaced helpers
+        me = self
+
+        def map_wid(mapping, wid, B, Hq, NB, NX):
+            N = B * Hq * NB
+            if not 0 <= wid < N:
+                raise ValueError("wid out of range")
+            if mapping == mp.NAIVE_BLOCK_FIRST:
+                b, mm, hq = me.unravel(wid, me.bf_radices(B, Hq, NB))
+                return b, hq, mm
+            if mapping == mp.NAIVE_HEAD_FIRST:
+                return me.unravel(wid, (B, Hq, NB))
+            return me.unravel(me.swizzled_rank(wid, N, NX), (B, Hq, NB))
+        self.map_wid = overrides.get("map_wid", map_wid)
+        self.__dict__.setdefault("bf_radices", lambda B, Hq, NB: (B, NB, Hq))
+
+
+def _unravel_first_fastest(x, radices):
+    digits = []
+    for r in radices:
+        digits.append(x % r)
+        x //= r
+    return tuple(digits)
+
+
+def _rank_no_ragged_term(wid, N, NX):
+    return (wid % NX) * (N // NX) + wid // NX
+
+
+def _rank_floor_ceil_swap(wid, N, NX):
+    q = -(-N // NX)
+    return (wid % NX) * q + wid // NX if (wid % NX) * q + wid // NX < N else wid
+
+
+MAP_MUTANTS = {
+    "unravel_first_digit_fastest": dict(unravel=_unravel_first_fastest),
+    "swizzle_without_ragged_term": dict(swizzled_rank=_rank_no_ragged_term),
+    "swizzle_ceil_stride": dict(swizzled_rank=_rank_floor_ceil_swap),
+    "swizzle_identity": dict(swizzled_rank=lambda wid, N, NX: wid),
+    "block_first_head_outer": dict(bf_radices=lambda B, Hq, NB: (B, Hq, NB)),
+    "floor_row_blocks": dict(num_row_blocks=lambda Sq, BM: Sq // BM),
+}
+
+
+def test_mutant_harness_is_faithful():
+    m = _Mutant()
+    for pin in PINS:
+        pin(m)
+
+
+@pytest.mark.parametrize("name", sorted(MAP_MUTANTS))
+def test_planted_mistake_is_caught(name):
+    m = _Mutant(**MAP_MUTANTS[name])
+    caught = []
+    for pin in PINS:
+        try:
+            pin(m)
+        except (AssertionError, ValueError, ZeroDivisionError, IndexError):
+            caught.append(pin.__name__)
+    assert caught, "planted mistake %s passed every pin" % name
