@@ -1,0 +1,134 @@
+/*
+ * attn_numa.h -- C ABI of the MI355X (gfx950) attention-forward library
+ * libattn_numa.so.
+ *
+ * The library computes the attention forward pass of Section 2.3, Eq. (1)
+ * ("eq:fa") with the FlashAttention-2 work split of Section 2.3.1: one
+ * workgroup (WG) per (batch, query head, block of BLOCK_M query rows), each WG
+ * streaming the whole K and V of its head.  The WG -> XCD placement is chosen
+ * by `mapping` (Sections 3.2 and 3.3):
+ *
+ *   ATTN_MAP_NAIVE_BLOCK_FIRST   -- block-major order (Section 3.2)
+ *   ATTN_MAP_NAIVE_HEAD_FIRST    -- head-major order (Section 3.2)
+ *   ATTN_MAP_SWIZZLED_HEAD_FIRST -- head-major order cut into one contiguous
+ *                                   piece per XCD (Section 3.3, the method)
+ *
+ * The hardware dispatches WG `wid` to XCD `wid mod NX` (Section 2.2); each
+ * mapping is a permutation wid -> (b, hq, m) computed in the kernel prologue.
+ * The output does not depend on the mapping (bitwise).
+ *
+ * No C++ types, exceptions or torch types cross this boundary.  Every entry
+ * point returns an int status (ATTN_OK or a negative ATTN_ERR_* code) unless
+ * stated otherwise; arguments are validated on the host before any HIP call.
+ */
+#ifndef ATTN_NUMA_H
+#define ATTN_NUMA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    ATTN_MAP_NAIVE_BLOCK_FIRST = 0,
+    ATTN_MAP_NAIVE_HEAD_FIRST = 1,
+    ATTN_MAP_SWIZZLED_HEAD_FIRST = 2
+};
+
+enum {
+    ATTN_OK = 0,
+    ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
+    ATTN_ERR_SHAPE = -2,       /* a dimension <= 0, Hq % Hkv != 0, or a size limit exceeded */
+    ATTN_ERR_UNSUPPORTED = -3, /* head dimension other than 64 or 128 */
+    ATTN_ERR_MAPPING = -4,     /* mapping not one of ATTN_MAP_* */
+    ATTN_ERR_SCALE = -5,       /* scale not finite or not > 0 */
+    ATTN_ERR_ALIGN = -6,       /* a tensor pointer not 16-byte aligned */
+    ATTN_ERR_HIP = -7,         /* a HIP runtime call failed; see attn_last_hip_error() */
+    ATTN_ERR_ALIAS = -8        /* o overlaps q, k or v */
+};
+
+/*
+ * attn_fwd -- attention forward, Section 2.3 Eq. (1) with GQA (Section 2.3,
+ * MHA/GQA paragraph) and an optional causal mask:
+ *
+ *   O[b,h,i,:] = sum_j softmax_j( scale * <Q[b,h,i,:], K[b,g,j,:]> ) * V[b,g,j,:]
+ *   g = h / (Hq / Hkv)      (contiguous groups of query heads share a K/V head)
+ *   causal: j ranges over 0..min(i, Skv-1) (top-left aligned); else 0..Skv-1
+ *
+ * q : device pointer, bf16, [B][Hq][Sq][d] contiguous, 16-byte aligned
+ * k : device pointer, bf16, [B][Hkv][Skv][d] contiguous, 16-byte aligned
+ * v : device pointer, bf16, [B][Hkv][Skv][d] contiguous, 16-byte aligned
+ * o : device pointer, bf16, [B][Hq][Sq][d] contiguous, 16-byte aligned;
+ *     must not overlap q, k or v.  Every element is written.
+ * d : 64 or 128.  Sq*d*2 and Skv*d*2 must each be below 2^31 bytes, and the
+ *     grid B*Hq*ceil(Sq/BLOCK_M) below 2^31.
+ * scale : finite and > 0 (the paper uses 1/sqrt(d)); softmax is taken in fp32
+ *     with bf16 inputs, fp32 accumulation and bf16 rounding (RNE) of P and O.
+ * mapping : one of ATTN_MAP_*.
+ *
+ * Ownership: all buffers belong to the caller; nothing is retained after the
+ * call returns and nothing is allocated.  The kernel is enqueued on the stream
+ * set by attn_set_stream() for the calling thread (default: the null stream)
+ * and the call returns without waiting; the caller synchronises.
+ */
+int attn_fwd(const void *q, const void *k, const void *v, void *o,
+             int B, int Hq, int Hkv, int Sq, int Skv, int d,
+             int causal, float scale, int mapping);
+
+/*
+ * attn_fwd_probe -- attn_fwd plus a record of the placement (Sections 2.2,
+ * 3.2, 3.3): the same kernel writes, for every workgroup id wid, four int32
+ * values probe[4*wid + 0..3] = (b, hq, m, xcc) where (b, hq, m) is the tile
+ * that WG computed and xcc the XCD it ran on (hardware register XCC_ID).
+ * probe : device pointer to attn_grid_size(B, Hq, Sq, d) * 4 int32, owned by
+ * the caller.  Other arguments and behaviour as attn_fwd.
+ */
+int attn_fwd_probe(const void *q, const void *k, const void *v, void *o,
+                   int B, int Hq, int Hkv, int Sq, int Skv, int d,
+                   int causal, float scale, int mapping, int32_t *probe);
+
+/* Number of workgroups attn_fwd launches: B * Hq * ceil(Sq / attn_block_m(d)),
+ * or a negative ATTN_ERR_* code for an invalid shape. */
+int64_t attn_grid_size(int B, int Hq, int Sq, int d);
+
+/*
+ * attn_map_tiles -- the placement the kernel uses, evaluated on the host by the
+ * same integer code the kernel prologue runs (Sections 3.2 and 3.3): for
+ * wid = 0 .. N-1, N = B*Hq*ceil(Sq/attn_block_m(d)), writes
+ * out[3*wid + 0..2] = (b, hq, m) of workgroup wid under `mapping` with NX XCDs.
+ * out : host pointer to N*3 int32, owned by the caller.  No HIP call is made.
+ */
+int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *out);
+
+/* Query rows per workgroup (BLOCK_M, Section 4.3) for head dimension d, or
+ * ATTN_ERR_UNSUPPORTED. */
+int attn_block_m(int d);
+
+/* Keys per K/V tile of the inner loop (BLOCK_N, Section 4.3) for head
+ * dimension d, or ATTN_ERR_UNSUPPORTED. */
+int attn_block_n(int d);
+
+/* XCD count NX that the mappings use: the ATTN_NUM_XCD environment variable
+ * when set to a positive integer, else hipDeviceAttributeNumberOfXccs of the
+ * current device (cached per device).  Negative ATTN_ERR_* on failure. */
+int attn_num_xcd(void);
+
+/* Stream for subsequent calls from the calling thread (a hipStream_t; NULL is
+ * the null stream).  The library does not take ownership. */
+int attn_set_stream(void *hip_stream);
+
+/* Stream currently set for the calling thread. */
+void *attn_get_stream(void);
+
+/* Static description of a status code (never NULL). */
+const char *attn_strerror(int code);
+
+/* Text of the last HIP error seen by the calling thread ("" if none). */
+const char *attn_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_NUMA_H */

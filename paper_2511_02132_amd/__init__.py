@@ -1,0 +1,185 @@
+"""Python binding of libattn_numa.so: NUMA-aware fused attention forward on MI355X.
+
+Argument marshalling only.  Every step of the computation runs in the HIP
+kernels of ``csrc/``; there is no CPU fallback, and a missing library is an
+error.  Torch provides device memory and streams.
+
+    from paper_2511_02132_amd import attn_fwd, SWIZZLED_HEAD_FIRST
+    o = attn_fwd(q, k, v, causal=True, mapping=SWIZZLED_HEAD_FIRST)
+
+q: [B, Hq, Sq, d], k/v: [B, Hkv, Skv, d], bf16, contiguous, on the GPU;
+d in {64, 128}; Hq a multiple of Hkv (grouped-query attention).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import numpy as np
+
+NAIVE_BLOCK_FIRST = 0
+NAIVE_HEAD_FIRST = 1
+SWIZZLED_HEAD_FIRST = 2
+MAPPINGS = {"naive_block_first": NAIVE_BLOCK_FIRST, "naive_head_first": NAIVE_HEAD_FIRST,
+            "swizzled_head_first": SWIZZLED_HEAD_FIRST}
+
+ATTN_OK = 0
+ATTN_ERR = {-1: "ATTN_ERR_NULL", -2: "ATTN_ERR_SHAPE", -3: "ATTN_ERR_UNSUPPORTED",
+            -4: "ATTN_ERR_MAPPING", -5: "ATTN_ERR_SCALE", -6: "ATTN_ERR_ALIGN",
+            -7: "ATTN_ERR_HIP", -8: "ATTN_ERR_ALIAS"}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libattn_numa.so")
+
+# Every symbol include/attn_numa.h declares, with its ctypes signature.
+_vp, _ci, _cf = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+_i32p = ctypes.POINTER(ctypes.c_int32)
+SIGNATURES = {
+    "attn_fwd": ([_vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
+    "attn_fwd_probe": ([_vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci, _vp],
+                       _ci),
+    "attn_grid_size": ([_ci, _ci, _ci, _ci], ctypes.c_int64),
+    "attn_map_tiles": ([_ci, _ci, _ci, _ci, _ci, _ci, _i32p], _ci),
+    "attn_block_m": ([_ci], _ci),
+    "attn_block_n": ([_ci], _ci),
+    "attn_num_xcd": ([], _ci),
+    "attn_set_stream": ([_vp], _ci),
+    "attn_get_stream": ([], _vp),
+    "attn_strerror": ([_ci], ctypes.c_char_p),
+    "attn_last_hip_error": ([], ctypes.c_char_p),
+}
+
+_lib = None
+
+
+class AttnError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(what)
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded, typed library.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("%s is missing: build it with `python -m paper_2511_02132_amd.build`"
+                              % LIB_PATH)
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (argtypes, restype) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.argtypes = argtypes
+            fn.restype = restype
+        _lib = handle
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return lib().attn_strerror(code).decode()
+
+
+def _check(rc: int, what: str) -> int:
+    if rc < 0:
+        msg = "%s failed: %s (%s)" % (what, ATTN_ERR.get(rc, rc), strerror(rc))
+        if rc == -7:
+            msg += ": " + lib().attn_last_hip_error().decode()
+        raise AttnError(rc, msg)
+    return rc
+
+
+def block_m(d: int) -> int:
+    return _check(lib().attn_block_m(d), "attn_block_m")
+
+
+def block_n(d: int) -> int:
+    return _check(lib().attn_block_n(d), "attn_block_n")
+
+
+def grid_size(B: int, Hq: int, Sq: int, d: int) -> int:
+    return _check(lib().attn_grid_size(B, Hq, Sq, d), "attn_grid_size")
+
+
+def num_xcd() -> int:
+    return _check(lib().attn_num_xcd(), "attn_num_xcd")
+
+
+def map_tiles(mapping: int, B: int, Hq: int, Sq: int, d: int, NX: int) -> np.ndarray:
+    """[N, 3] int32 (b, hq, m) per workgroup id, from the library's own mapping code."""
+    n = grid_size(B, Hq, Sq, d)
+    out = np.empty((n, 3), dtype=np.int32)
+    _check(lib().attn_map_tiles(mapping, B, Hq, Sq, d, NX, out.ctypes.data_as(_i32p)),
+           "attn_map_tiles")
+    return out
+
+
+def _shapes(q, k, v, o):
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError("%s must be a torch.Tensor" % name)
+        if t.dtype != torch.bfloat16:
+            raise TypeError("%s must be bfloat16, got %s" % (name, t.dtype))
+        if t.device.type != "cuda":
+            raise ValueError("%s must be on the GPU, got %s" % (name, t.device))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous (BHSD)" % name)
+        if t.dim() != 4:
+            raise ValueError("%s must be 4-D [B, H, S, d]" % name)
+    B, Hq, Sq, d = q.shape
+    Bk, Hkv, Skv, dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or Bk != B or dk != d:
+        raise ValueError("k and v must be [B, Hkv, Skv, d] matching q")
+    if tuple(o.shape) != tuple(q.shape):
+        raise ValueError("o must have q's shape")
+    if not (q.device == k.device == v.device == o.device):
+        raise ValueError("all tensors must be on one device")
+    return B, Hq, Hkv, Sq, Skv, d
+
+
+def _prepare(q, k, v, o, scale, stream):
+    import torch
+    if o is None:
+        o = torch.empty_like(q)
+    B, Hq, Hkv, Sq, Skv, d = _shapes(q, k, v, o)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    torch.cuda.set_device(q.device)
+    lib().attn_set_stream(ctypes.c_void_p(stream.cuda_stream))
+    return o, (B, Hq, Hkv, Sq, Skv, d), float(scale)
+
+
+def attn_fwd(q, k, v, o=None, *, causal: bool = False, scale: float | None = None,
+             mapping: int = SWIZZLED_HEAD_FIRST, stream=None):
+    """O = softmax(scale * Q K^T [causal]) V on the GPU; returns o (enqueued, not synced)."""
+    o, (B, Hq, Hkv, Sq, Skv, d), scale = _prepare(q, k, v, o, scale, stream)
+    _check(lib().attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                          B, Hq, Hkv, Sq, Skv, d, int(bool(causal)), scale, int(mapping)),
+           "attn_fwd")
+    return o
+
+
+def attn_fwd_probe(q, k, v, o=None, probe=None, *, causal: bool = False,
+                   scale: float | None = None, mapping: int = SWIZZLED_HEAD_FIRST, stream=None):
+    """attn_fwd plus the per-workgroup record [N, 4] int32 = (b, hq, m, xcc)."""
+    import torch
+    o, (B, Hq, Hkv, Sq, Skv, d), scale = _prepare(q, k, v, o, scale, stream)
+    n = grid_size(B, Hq, Sq, d)
+    if probe is None:
+        probe = torch.full((n, 4), -1, dtype=torch.int32, device=q.device)
+    if probe.dtype != torch.int32 or probe.numel() < 4 * n or not probe.is_contiguous() \
+            or probe.device != q.device:
+        raise ValueError("probe must be a contiguous int32 GPU tensor with >= 4*N elements")
+    _check(lib().attn_fwd_probe(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                B, Hq, Hkv, Sq, Skv, d, int(bool(causal)), scale, int(mapping),
+                                probe.data_ptr()),
+           "attn_fwd_probe")
+    return o, probe
+
+
+def attention_flops(B: int, Hq: int, Sq: int, Skv: int, d: int, causal: bool) -> float:
+    """FlashAttention convention: 4*B*Hq*Sq*Skv*d, halved when causal."""
+    f = 4.0 * B * Hq * Sq * Skv * d
+    return f / 2 if causal else f

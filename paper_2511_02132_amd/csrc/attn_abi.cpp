@@ -1,0 +1,190 @@
+// attn_abi.cpp -- the C ABI of libattn_numa.so: argument validation, status
+// codes, per-thread stream, XCD count, and the launch of the forward kernel.
+// Every check runs on the host before the first HIP call, so invalid calls
+// fail the same way with or without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "attn_internal.h"
+#include "attn_numa.h"
+
+namespace {
+
+thread_local hipStream_t t_stream = nullptr;
+thread_local char t_hip_error[256] = "";
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_nx_cache[kMaxDevices];   // 0 = not yet queried
+
+int hip_fail(hipError_t e) {
+    std::snprintf(t_hip_error, sizeof t_hip_error, "%s (%d)", hipGetErrorString(e), (int)e);
+    return ATTN_ERR_HIP;
+}
+
+bool supported_d(int d) { return d == 64 || d == 128; }
+
+// Shape checks shared by every entry point.  Offsets inside one head are
+// 32-bit byte offsets, so a head (plus one tile of slack) must stay below 2^31.
+int check_shape(int B, int Hq, int Hkv, int Sq, int Skv, int d) {
+    if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Skv <= 0 || d <= 0) return ATTN_ERR_SHAPE;
+    if (Hq % Hkv != 0) return ATTN_ERR_SHAPE;
+    if (!supported_d(d)) return ATTN_ERR_UNSUPPORTED;
+    const int64_t lim = INT32_MAX;
+    if (((int64_t)Sq + attn::kBlockM) * d * 2 > lim) return ATTN_ERR_SHAPE;
+    if (((int64_t)Skv + attn::kBlockN) * d * 2 > lim) return ATTN_ERR_SHAPE;
+    const int64_t nb = ((int64_t)Sq + attn::kBlockM - 1) / attn::kBlockM;
+    if ((int64_t)B * Hq * nb > lim) return ATTN_ERR_SHAPE;
+    return ATTN_OK;
+}
+
+bool overlaps(const void *a, int64_t a_bytes, const void *b, int64_t b_bytes) {
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + (uintptr_t)b_bytes && b0 < a0 + (uintptr_t)a_bytes;
+}
+
+int validate(const void *q, const void *k, const void *v, const void *o, int B, int Hq, int Hkv,
+             int Sq, int Skv, int d, float scale, int mapping) {
+    if (!q || !k || !v || !o) return ATTN_ERR_NULL;
+    int rc = check_shape(B, Hq, Hkv, Sq, Skv, d);
+    if (rc) return rc;
+    if (mapping != ATTN_MAP_NAIVE_BLOCK_FIRST && mapping != ATTN_MAP_NAIVE_HEAD_FIRST &&
+        mapping != ATTN_MAP_SWIZZLED_HEAD_FIRST)
+        return ATTN_ERR_MAPPING;
+    if (!std::isfinite(scale) || !(scale > 0.0f)) return ATTN_ERR_SCALE;
+    if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o) & 15u) return ATTN_ERR_ALIGN;
+    const int64_t qo_bytes = (int64_t)B * Hq * Sq * d * 2;
+    const int64_t kv_bytes = (int64_t)B * Hkv * Skv * d * 2;
+    if (overlaps(o, qo_bytes, q, qo_bytes) || overlaps(o, qo_bytes, k, kv_bytes) ||
+        overlaps(o, qo_bytes, v, kv_bytes))
+        return ATTN_ERR_ALIAS;
+    return ATTN_OK;
+}
+
+int env_num_xcd() {
+    const char *s = std::getenv("ATTN_NUM_XCD");
+    if (!s || !*s) return 0;
+    char *end = nullptr;
+    const long v = std::strtol(s, &end, 10);
+    if (end == s || *end != '\0' || v <= 0 || v > 64) return 0;
+    return (int)v;
+}
+
+int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv, int Sq,
+        int Skv, int d, int causal, float scale, int mapping, int32_t *probe) {
+    int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
+    if (rc) return rc;
+    const int nx = attn_num_xcd();
+    if (nx < 0) return nx;
+    attn::KernelArgs a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.probe = probe;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.Sq = Sq;
+    a.Skv = Skv;
+    a.NB = (Sq + attn::kBlockM - 1) / attn::kBlockM;
+    a.NX = nx;
+    a.mapping = mapping;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
+    const int grid = B * Hq * a.NB;
+    hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, grid, t_stream);
+    if (e != hipSuccess) return hip_fail(e);
+    return ATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int attn_fwd(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv, int Sq,
+             int Skv, int d, int causal, float scale, int mapping) {
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, nullptr);
+}
+
+int attn_fwd_probe(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv,
+                   int Sq, int Skv, int d, int causal, float scale, int mapping, int32_t *probe) {
+    if (!probe) return ATTN_ERR_NULL;
+    if (((uintptr_t)probe) & 3u) return ATTN_ERR_ALIGN;
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe);
+}
+
+int64_t attn_grid_size(int B, int Hq, int Sq, int d) {
+    if (B <= 0 || Hq <= 0 || Sq <= 0 || d <= 0) return ATTN_ERR_SHAPE;
+    if (!supported_d(d)) return ATTN_ERR_UNSUPPORTED;
+    return (int64_t)B * Hq * (((int64_t)Sq + attn::kBlockM - 1) / attn::kBlockM);
+}
+
+int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *out) {
+    if (!out) return ATTN_ERR_NULL;
+    if (mapping != ATTN_MAP_NAIVE_BLOCK_FIRST && mapping != ATTN_MAP_NAIVE_HEAD_FIRST &&
+        mapping != ATTN_MAP_SWIZZLED_HEAD_FIRST)
+        return ATTN_ERR_MAPPING;
+    if (NX <= 0) return ATTN_ERR_SHAPE;
+    const int64_t n = attn_grid_size(B, Hq, Sq, d);
+    if (n < 0) return (int)n;
+    if (n > INT32_MAX) return ATTN_ERR_SHAPE;
+    const int nb = (Sq + attn::kBlockM - 1) / attn::kBlockM;
+    for (int64_t wid = 0; wid < n; ++wid) {
+        const attn::Tile t = attn::map_wid(mapping, (int)wid, B, Hq, nb, NX);
+        out[3 * wid + 0] = t.b;
+        out[3 * wid + 1] = t.hq;
+        out[3 * wid + 2] = t.m;
+    }
+    return ATTN_OK;
+}
+
+int attn_block_m(int d) { return supported_d(d) ? attn::kBlockM : ATTN_ERR_UNSUPPORTED; }
+
+int attn_block_n(int d) { return supported_d(d) ? attn::kBlockN : ATTN_ERR_UNSUPPORTED; }
+
+int attn_num_xcd(void) {
+    const int env = env_num_xcd();
+    if (env > 0) return env;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (dev < 0 || dev >= kMaxDevices) return ATTN_ERR_UNSUPPORTED;
+    int nx = g_nx_cache[dev].load(std::memory_order_relaxed);
+    if (nx > 0) return nx;
+    e = hipDeviceGetAttribute(&nx, hipDeviceAttributeNumberOfXccs, dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (nx <= 0) nx = 1;
+    g_nx_cache[dev].store(nx, std::memory_order_relaxed);
+    return nx;
+}
+
+int attn_set_stream(void *hip_stream) {
+    t_stream = (hipStream_t)hip_stream;
+    return ATTN_OK;
+}
+
+void *attn_get_stream(void) { return (void *)t_stream; }
+
+const char *attn_strerror(int code) {
+    switch (code) {
+        case ATTN_OK: return "ok";
+        case ATTN_ERR_NULL: return "null pointer argument";
+        case ATTN_ERR_SHAPE: return "invalid shape (non-positive dimension, Hq % Hkv != 0, or size limit)";
+        case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (supported: 64, 128)";
+        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first)";
+        case ATTN_ERR_SCALE: return "scale must be finite and > 0";
+        case ATTN_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
+        case ATTN_ERR_HIP: return "HIP runtime error";
+        case ATTN_ERR_ALIAS: return "output overlaps an input";
+        default: return "unknown status code";
+    }
+}
+
+const char *attn_last_hip_error(void) { return t_hip_error; }
+
+}  // extern "C"

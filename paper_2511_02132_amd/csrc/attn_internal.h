@@ -1,0 +1,67 @@
+// attn_internal.h -- declarations shared by the host launcher and the kernels
+// of libattn_numa.so (not part of the public C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace attn {
+
+// Query rows per workgroup and keys per K/V tile (Section 4.3 uses 128 x 64).
+constexpr int kBlockM = 128;
+constexpr int kBlockN = 64;
+
+// Kernel arguments; tensors are bf16, BHSD contiguous.
+struct KernelArgs {
+    const void *q;
+    const void *k;
+    const void *v;
+    void *o;
+    int32_t *probe;   // NULL, or 4 int32 per workgroup: b, hq, m, xcc
+    int B, Hq, Hkv, Sq, Skv;
+    int NB;           // ceil(Sq / kBlockM)
+    int NX;           // XCD count used by the mapping
+    int mapping;      // ATTN_MAP_*
+    float scale_log2; // scale * log2(e): softmax evaluated with exp2
+};
+
+struct Tile {
+    int b, hq, m;
+};
+
+// Workgroup id -> tile (b, hq, m) for mapping 0/1/2 (ATTN_MAP_*); integer only.
+// In the kernel the arguments are uniform, so this runs on the scalar unit.
+//   0 naive block-first:   digits of wid over (B, NB, Hq), heads fastest
+//   1 naive head-first:    digits of wid over (B, Hq, NB), blocks fastest
+//   2 swizzled head-first: digits over (B, Hq, NB) of the rank of wid in the
+//     XCD-major listing of the grid (XCD x = wid mod NX receives its k-th WG
+//     as wid = x + k*NX; the first N mod NX XCDs hold one WG more).
+__host__ __device__ inline Tile map_wid(int mapping, int wid, int B, int Hq, int NB, int NX) {
+    Tile t;
+    if (mapping == 0) {
+        t.hq = wid % Hq;
+        const int rest = wid / Hq;
+        t.m = rest % NB;
+        t.b = rest / NB;
+        return t;
+    }
+    int L = wid;
+    if (mapping == 2) {
+        const int N = B * Hq * NB;
+        const int x = wid % NX;
+        const int k = wid / NX;
+        const int q = N / NX;
+        const int r = N % NX;
+        L = x * q + (x < r ? x : r) + k;
+    }
+    t.m = L % NB;
+    const int rest = L / NB;
+    t.hq = rest % Hq;
+    t.b = rest / Hq;
+    return t;
+}
+
+// Enqueue the forward kernel for head dimension d (64 or 128).
+hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int grid, hipStream_t stream);
+
+}  // namespace attn

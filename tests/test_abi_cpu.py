@@ -1,0 +1,117 @@
+"""CPU-only checks of the C ABI of libattn_numa.so (no GPU, no kernel launch).
+
+* the library loads and exports every function include/attn_numa.h declares;
+* argument validation returns the documented status codes before any HIP
+  call (fake, never dereferenced pointers);
+* the library's own mapping code (the integer code the kernel prologue runs,
+  evaluated on the host by attn_map_tiles) equals the oracle enumeration on
+  many shapes, so every workgroup's (b, hq, m) is in range before the kernel
+  ever runs on a GPU.
+"""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2511_02132_amd as pa
+from oracle import mapping as mp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "attn_numa.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(attn_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = pa.lib()
+    names = header_functions()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(pa.SIGNATURES) == names
+
+
+# fake device addresses: 16-byte aligned, never dereferenced
+Q, K, V, O = 0x10000000, 0x20000000, 0x30000000, 0x40000000
+
+
+def call(q=Q, k=K, v=V, o=O, B=1, Hq=4, Hkv=2, Sq=256, Skv=256, d=128, causal=0, scale=0.088,
+         mapping=2):
+    return pa.lib().attn_fwd(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping)
+
+
+@pytest.mark.parametrize("kwargs,code", [
+    (dict(q=None), -1), (dict(k=None), -1), (dict(v=None), -1), (dict(o=None), -1),
+    (dict(B=0), -2), (dict(Hq=0), -2), (dict(Hkv=0), -2), (dict(Sq=0), -2), (dict(Skv=-1), -2),
+    (dict(Hq=6, Hkv=4), -2), (dict(Sq=2 ** 23), -2), (dict(Skv=2 ** 23), -2),
+    (dict(d=96), -3), (dict(d=256), -3), (dict(d=0), -2),
+    (dict(mapping=3), -4), (dict(mapping=-1), -4),
+    (dict(scale=float("nan")), -5), (dict(scale=float("inf")), -5), (dict(scale=0.0), -5),
+    (dict(scale=-1.0), -5),
+    (dict(q=Q + 8), -6), (dict(o=O + 2), -6),
+    (dict(o=Q), -8), (dict(o=K + 256), -8),
+])
+def test_validation_codes(kwargs, code):
+    assert call(**kwargs) == code
+    assert pa.strerror(code) and pa.strerror(code) != "unknown status code"
+
+
+def test_probe_validation():
+    lib = pa.lib()
+    args = (Q, K, V, O, 1, 4, 2, 256, 256, 128, 0, 0.088, 2)
+    assert lib.attn_fwd_probe(*args, None) == -1
+    assert lib.attn_fwd_probe(*args, 0x50000002) == -6
+    bad = (Q, K, V, O, 1, 4, 3, 256, 256, 128, 0, 0.088, 2)
+    assert lib.attn_fwd_probe(*bad, 0x50000000) == -2
+
+
+def test_sizes():
+    assert pa.block_m(64) == pa.block_m(128) == 128
+    assert pa.block_n(64) == pa.block_n(128) == 64
+    assert pa.lib().attn_block_m(96) == -3
+    assert pa.grid_size(1, 32, 8192, 128) == 2048
+    assert pa.grid_size(8, 64, 4096, 128) == 16384
+    assert pa.grid_size(2, 3, 129, 64) == 12
+    assert pa.lib().attn_grid_size(1, 1, 0, 128) == -2
+
+
+def test_num_xcd_env_override(monkeypatch):
+    monkeypatch.setenv("ATTN_NUM_XCD", "4")
+    assert pa.num_xcd() == 4
+
+
+def test_stream_roundtrip():
+    lib = pa.lib()
+    assert lib.attn_set_stream(0x1234) == 0
+    assert lib.attn_get_stream() == 0x1234
+    assert lib.attn_set_stream(None) == 0
+    assert lib.attn_get_stream() is None
+    assert lib.attn_last_hip_error() == b""
+
+
+MAP_SHAPES = [(1, 4, 256, 64, 8), (1, 32, 8192, 128, 8), (1, 64, 8192, 128, 8),
+              (8, 64, 4096, 128, 8), (1, 16, 131072, 128, 8), (2, 12, 300, 128, 8),
+              (3, 5, 1000, 64, 4), (1, 1, 1, 128, 8), (2, 3, 129, 64, 1), (1, 8, 16384, 128, 8)]
+
+
+@pytest.mark.parametrize("B,Hq,Sq,d,NX", MAP_SHAPES)
+def test_library_mapping_equals_oracle(B, Hq, Sq, d, NX):
+    BM = pa.block_m(d)
+    for mapping in (0, 1, 2):
+        got = pa.map_tiles(mapping, B, Hq, Sq, d, NX)
+        want = mp.enumerate_mapping(mapping, B, Hq, Sq, BM, NX)
+        assert np.array_equal(got, want), mapping
+
+
+def test_map_tiles_errors():
+    assert pa.lib().attn_map_tiles(2, 1, 4, 256, 64, 8, None) == -1
+    out = np.empty(8 * 3, np.int32)
+    ptr = out.ctypes.data_as(pa._i32p)
+    assert pa.lib().attn_map_tiles(5, 1, 4, 256, 64, 8, ptr) == -4
+    assert pa.lib().attn_map_tiles(2, 1, 4, 256, 64, 0, ptr) == -2
