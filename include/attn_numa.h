@@ -33,7 +33,14 @@ extern "C" {
 enum {
     ATTN_MAP_NAIVE_BLOCK_FIRST = 0,
     ATTN_MAP_NAIVE_HEAD_FIRST = 1,
-    ATTN_MAP_SWIZZLED_HEAD_FIRST = 2
+    ATTN_MAP_SWIZZLED_HEAD_FIRST = 2,
+    /* Optional flag OR-ed into any mapping: dispatch each head's row blocks
+     * from the last to the first (m -> NB-1-m).  The XCD that runs each
+     * (batch, head) is unchanged; under a causal mask, where block m costs m+1
+     * K/V tiles, the expensive blocks start first and the tail shrinks.  Not
+     * part of the paper's mappings (Sections 3.2, 3.3), which dispatch blocks
+     * in increasing order. */
+    ATTN_ORDER_HEAVY_FIRST = 0x10
 };
 
 enum {
@@ -65,7 +72,8 @@ enum {
  *     grid B*Hq*ceil(Sq/BLOCK_M) below 2^31.
  * scale : finite and > 0 (the paper uses 1/sqrt(d)); softmax is taken in fp32
  *     with bf16 inputs, fp32 accumulation and bf16 rounding (RNE) of P and O.
- * mapping : one of ATTN_MAP_*.
+ * mapping : one of ATTN_MAP_NAIVE_BLOCK_FIRST, ATTN_MAP_NAIVE_HEAD_FIRST,
+ *     ATTN_MAP_SWIZZLED_HEAD_FIRST, optionally | ATTN_ORDER_HEAVY_FIRST.
  *
  * Ownership: all buffers belong to the caller; nothing is retained after the
  * call returns and nothing is allocated.  The kernel is enqueued on the stream

@@ -33,6 +33,11 @@ The three mappings (integer ``mapping`` argument of the C ABI):
      not, where the first r XCDs take one WG more.  Batch is outermost
      throughout (the readings of the garbled per-batch line of the listing and
      of Hq < NX are recorded with the design notes).
+
+Order option (not one of the paper's mappings): ``heavy_first`` replaces the
+row block m by NB-1-m after any mapping, so every (b, hq) keeps its XCD but
+each head's blocks are dispatched last-to-first.  Under a causal mask block m
+costs m+1 K/V tiles, so this starts the expensive blocks first.
 """
 
 from __future__ import annotations
@@ -77,7 +82,8 @@ def swizzled_rank(wid: int, N: int, NX: int) -> int:
     return x * q + min(x, r) + k
 
 
-def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int) -> tuple:
+def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
+            heavy_first: bool = False) -> tuple:
     """(b, hq, m) that WG ``wid`` computes under ``mapping``."""
     N = B * Hq * NB
     if not 0 <= wid < N:
@@ -90,16 +96,19 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int) -> tuple:
         b, hq, m = unravel(swizzled_rank(wid, N, NX), (B, Hq, NB))
     else:
         raise ValueError("unknown mapping %r" % (mapping,))
+    if heavy_first:
+        m = NB - 1 - m
     return b, hq, m
 
 
-def enumerate_mapping(mapping: int, B: int, Hq: int, Sq: int, BM: int, NX: int) -> np.ndarray:
+def enumerate_mapping(mapping: int, B: int, Hq: int, Sq: int, BM: int, NX: int,
+                      heavy_first: bool = False) -> np.ndarray:
     """Array [N, 3] of (b, hq, m) for wid = 0 .. N-1 (pure-Python loop)."""
     NB = num_row_blocks(Sq, BM)
     N = B * Hq * NB
     out = np.empty((N, 3), dtype=np.int64)
     for wid in range(N):
-        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX)
+        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX, heavy_first)
     return out
 
 

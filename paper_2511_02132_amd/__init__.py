@@ -22,6 +22,8 @@ import numpy as np
 NAIVE_BLOCK_FIRST = 0
 NAIVE_HEAD_FIRST = 1
 SWIZZLED_HEAD_FIRST = 2
+# Flag OR-ed into a mapping: dispatch each head's row blocks last-to-first.
+HEAVY_FIRST = 0x10
 MAPPINGS = {"naive_block_first": NAIVE_BLOCK_FIRST, "naive_head_first": NAIVE_HEAD_FIRST,
             "swizzled_head_first": SWIZZLED_HEAD_FIRST}
 

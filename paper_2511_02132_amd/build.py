@@ -19,6 +19,20 @@ SOURCES = ["attn_fwd.hip", "attn_abi.cpp"]
 ARCH = "gfx950"
 
 
+KERNEL_SOURCES = ["attn_fwd.hip", "attn_internal.h"]
+
+
+def kernel_source_hash() -> str:
+    """Short hash of the kernel sources: ties a counter summary to the code it measured."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):

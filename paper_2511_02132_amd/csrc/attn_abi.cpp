@@ -43,6 +43,14 @@ int check_shape(int B, int Hq, int Hkv, int Sq, int Skv, int d) {
     return ATTN_OK;
 }
 
+// Base mapping in the low 4 bits, optional order flag above them.
+bool valid_mapping(int mapping) {
+    const int base = mapping & 0xf;
+    const int flags = mapping & ~0xf;
+    return base >= ATTN_MAP_NAIVE_BLOCK_FIRST && base <= ATTN_MAP_SWIZZLED_HEAD_FIRST &&
+           (flags & ~ATTN_ORDER_HEAVY_FIRST) == 0;
+}
+
 bool overlaps(const void *a, int64_t a_bytes, const void *b, int64_t b_bytes) {
     const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
     return a0 < b0 + (uintptr_t)b_bytes && b0 < a0 + (uintptr_t)a_bytes;
@@ -53,9 +61,7 @@ int validate(const void *q, const void *k, const void *v, const void *o, int B, 
     if (!q || !k || !v || !o) return ATTN_ERR_NULL;
     int rc = check_shape(B, Hq, Hkv, Sq, Skv, d);
     if (rc) return rc;
-    if (mapping != ATTN_MAP_NAIVE_BLOCK_FIRST && mapping != ATTN_MAP_NAIVE_HEAD_FIRST &&
-        mapping != ATTN_MAP_SWIZZLED_HEAD_FIRST)
-        return ATTN_ERR_MAPPING;
+    if (!valid_mapping(mapping)) return ATTN_ERR_MAPPING;
     if (!std::isfinite(scale) || !(scale > 0.0f)) return ATTN_ERR_SCALE;
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o) & 15u) return ATTN_ERR_ALIGN;
     const int64_t qo_bytes = (int64_t)B * Hq * Sq * d * 2;
@@ -94,10 +100,10 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.Skv = Skv;
     a.NB = (Sq + attn::kBlockM - 1) / attn::kBlockM;
     a.NX = nx;
-    a.mapping = mapping;
+    a.heavy_first = (mapping & ATTN_ORDER_HEAVY_FIRST) != 0;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
     const int grid = B * Hq * a.NB;
-    hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, grid, t_stream);
+    hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, mapping & 0xf, grid, t_stream);
     if (e != hipSuccess) return hip_fail(e);
     return ATTN_OK;
 }
@@ -126,16 +132,15 @@ int64_t attn_grid_size(int B, int Hq, int Sq, int d) {
 
 int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *out) {
     if (!out) return ATTN_ERR_NULL;
-    if (mapping != ATTN_MAP_NAIVE_BLOCK_FIRST && mapping != ATTN_MAP_NAIVE_HEAD_FIRST &&
-        mapping != ATTN_MAP_SWIZZLED_HEAD_FIRST)
-        return ATTN_ERR_MAPPING;
+    if (!valid_mapping(mapping)) return ATTN_ERR_MAPPING;
     if (NX <= 0) return ATTN_ERR_SHAPE;
     const int64_t n = attn_grid_size(B, Hq, Sq, d);
     if (n < 0) return (int)n;
     if (n > INT32_MAX) return ATTN_ERR_SHAPE;
     const int nb = (Sq + attn::kBlockM - 1) / attn::kBlockM;
     for (int64_t wid = 0; wid < n; ++wid) {
-        const attn::Tile t = attn::map_wid(mapping, (int)wid, B, Hq, nb, NX);
+        const attn::Tile t = attn::map_wid(mapping & 0xf, (mapping & ATTN_ORDER_HEAVY_FIRST) != 0,
+                                           (int)wid, B, Hq, nb, NX);
         out[3 * wid + 0] = t.b;
         out[3 * wid + 1] = t.hq;
         out[3 * wid + 2] = t.m;
@@ -176,7 +181,7 @@ const char *attn_strerror(int code) {
         case ATTN_ERR_NULL: return "null pointer argument";
         case ATTN_ERR_SHAPE: return "invalid shape (non-positive dimension, Hq % Hkv != 0, or size limit)";
         case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (supported: 64, 128)";
-        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first)";
+        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, optionally | ATTN_ORDER_HEAVY_FIRST)";
         case ATTN_ERR_SCALE: return "scale must be finite and > 0";
         case ATTN_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
         case ATTN_ERR_HIP: return "HIP runtime error";

@@ -35,12 +35,11 @@
 // so the softmax row reductions are lane-local except one exchange between
 // lanes l and l^32 per tile.
 //
-// LDS (double-buffered K and V tiles, 2 x 2 x 64 x d bf16): rows of K are
-// stored with 16-byte chunk c at position c ^ (row & 7), rows of V with
-// 32-byte segment s at position s ^ (row & 3); both make the MFMA operand reads
-// free of bank conflicts.  Global loads are 16-byte buffer loads whose
-// out-of-range lanes read zero (ragged Sq / Skv tails); stores out of range
-// are dropped.
+// LDS (double-buffered K and V tiles, 2 x 2 x 64 x d bf16) is filled directly
+// by buffer loads (no register staging): the copy of tile n+1 runs while tile
+// n is computed.  Rows are stored swizzled (see k_swizzle / v_swizzle) so that
+// the MFMA operand reads are free of bank conflicts.  Buffer loads out of
+// range read zero (ragged Sq / Skv tails); stores out of range are dropped.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -57,6 +56,7 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
@@ -66,6 +66,29 @@ typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 constexpr int kThreads = 256;
 // Word 3 of a gfx9 buffer resource: 32-bit data format, raw (stride 0) access.
 constexpr int kBufferFlags = 0x00020000;
+
+// Buffer resource as four scalar words (gfx9 layout): base address, stride 0,
+// size in bytes (accesses at or past it read zero / are dropped), flags.
+__device__ __forceinline__ i32x4 buffer_words(const void *base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)base;
+    i32x4 r;
+    r[0] = (int)(uint32_t)a;
+    r[1] = (int)(uint32_t)(a >> 32) & 0xffff;
+    r[2] = (int)bytes;
+    r[3] = kBufferFlags;
+    return r;
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane j's bytes land
+// at lds_addr + 16*j.  Issued from inline assembly so that the compiler does
+// not order later LDS reads of the other buffer behind it; the kernel waits for
+// these copies itself (vmcnt) before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_copy16(i32x4 rsrc, uint32_t voffset, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voffset), "s"(rsrc), "s"(lds_addr)
+                 : "memory", "m0");
+}
 
 __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t rsrc, uint32_t byte_off) {
     return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)byte_off, 0, 0);
@@ -78,28 +101,56 @@ __device__ __forceinline__ float xor32(float x) {
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int D, bool CAUSAL>
+// s_waitcnt operand: vmcnt(0), expcnt and lgkmcnt not waited for.
+constexpr int kWaitVmcnt0 = 0x0f70;
+
+// LDS swizzles.  gfx950 serves 16 lanes of a 16-byte read (or of the 8-byte
+// transposing read) from 64 four-byte banks, a 256-byte window; sixteen
+// consecutive rows must therefore land in sixteen distinct 16-byte bank groups.
+//   K rows (read as 16-byte chunks by 16 consecutive rows): chunk c of row r is
+//   stored at c ^ k_swizzle(r); for 128-byte rows two rows share a window.
+template <int D>
+__device__ __forceinline__ int k_swizzle(int row) {
+    return D == 128 ? (row & 15) : ((row >> 1) & 7);
+}
+//   V rows (read 4 rows x 32 bytes per 16 lanes, two such groups on adjacent
+//   segments per 32 lanes): 32-byte segment s of row r is stored at
+//   s ^ v_swizzle(r), which keeps all 8 (row, segment) pairs of 32 lanes apart.
+template <int D>
+__device__ __forceinline__ int v_swizzle(int row) {
+    return D == 128 ? 2 * (row & 3) : 2 * ((row >> 1) & 1);
+}
+
+template <int V>
+struct Int {
+    static constexpr int value = V;
+};
+
+// Lazy rescaling threshold (exp2 domain): probabilities stay below 2^8.
+constexpr float kLazy = 8.0f;
+
+template <int D, bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs p) {
     constexpr int BM = kBlockM;
     constexpr int BN = kBlockN;
     constexpr int KSTEPS = D / 16;             // MFMA k-steps of S^T = K Q^T
     constexpr int DBLK = D / 32;               // 32-row blocks of O^T
     constexpr int CHUNKS_PER_ROW = D / 8;      // 16-byte chunks per K/V row
-    constexpr int CPT = BN * CHUNKS_PER_ROW / kThreads;  // chunks per thread per tile
     constexpr int ROW_BYTES = D * 2;
     constexpr int TILE_BYTES = BN * ROW_BYTES;
-    static_assert(CPT * kThreads == BN * CHUNKS_PER_ROW, "tile not divisible");
+    constexpr int IPW = TILE_BYTES / 1024 / (kThreads / 64);   // LDS-copy instructions per wave
+    static_assert(IPW * 1024 * (kThreads / 64) == TILE_BYTES, "tile not divisible");
 
     __shared__ __attribute__((aligned(1024))) char smem[4 * TILE_BYTES];
     lds_char *const lds = (lds_char *)smem;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = tid >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, kept scalar
     const int c = lane & 31;   // query column of the MFMA tiles
     const int h = lane >> 5;   // which half of the 64 lanes
 
-    const Tile t = map_wid(p.mapping, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
+    const Tile t = map_wid(MAPPING, HEAVY_FIRST, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
     if (p.probe != nullptr && tid == 0) {
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
@@ -115,10 +166,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * D;
     const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
         (void *)((const char *)p.q + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)p.k + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)p.v + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
     const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
         (void *)((char *)p.o + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
 
@@ -131,66 +178,83 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         qreg[kk] = __builtin_bit_cast(
             bf16x8, load16(rq, (uint32_t)(my_q * D + 16 * kk + 8 * h) * 2u));
 
-    // Per-thread share of a K/V tile copy: global offsets and swizzled LDS slots.
-    uint32_t g_off[CPT], k_slot[CPT], v_slot[CPT];
+    // K/V tiles go straight from global memory to LDS (buffer_load ... lds):
+    // each instruction of a wave fills 1024 contiguous LDS bytes, lane j the
+    // 16 bytes at j*16, so the swizzled layout is made by choosing which
+    // global 16-byte chunk each lane fetches.  Wave w fills LDS slots
+    // (w*IPW + i)*64 + lane, i < IPW, of each tile.
+    uint32_t k_src[IPW], v_src[IPW];
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-        const int ci = tid + kThreads * i;
-        const int row = ci / CHUNKS_PER_ROW;
-        const int cc = ci % CHUNKS_PER_ROW;
-        g_off[i] = (uint32_t)(row * D + cc * 8) * 2u;
-        k_slot[i] = row * ROW_BYTES + ((cc ^ (row & 7)) * 16);
-        v_slot[i] = row * ROW_BYTES + ((((cc >> 1) ^ (row & 3)) * 2 + (cc & 1)) * 16);
+    for (int i = 0; i < IPW; ++i) {
+        const int slot = (w * IPW + i) * 64 + lane;
+        const int row = slot / CHUNKS_PER_ROW;
+        const int phys = slot % CHUNKS_PER_ROW;
+        k_src[i] = row * ROW_BYTES + ((phys ^ k_swizzle<D>(row)) * 16);
+        const int seg = (phys >> 1) ^ v_swizzle<D>(row);
+        v_src[i] = row * ROW_BYTES + (seg * 2 + (phys & 1)) * 16;
     }
+    const i32x4 wk = buffer_words((const char *)p.k + kv_head * 2, p.Skv * ROW_BYTES);
+    const i32x4 wv = buffer_words((const char *)p.v + kv_head * 2, p.Skv * ROW_BYTES);
+    const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+    auto issue_tile = [&](const int n, auto buf) {
+        constexpr int BUF = decltype(buf)::value;
+        const uint32_t tile = (uint32_t)n * TILE_BYTES;
+#pragma unroll
+        for (int i = 0; i < IPW; ++i) {
+            const uint32_t dst = lds_base + BUF * 2 * TILE_BYTES + (w * IPW + i) * 1024;
+            lds_copy16(wk, tile + k_src[i], dst);
+            lds_copy16(wv, tile + v_src[i], dst + TILE_BYTES);
+        }
+    };
 
     const int kv_end = CAUSAL ? min((t.m + 1) * BM, p.Skv) : p.Skv;
     const int n_tiles = (kv_end + BN - 1) / BN;
+    issue_tile(0, Int<0>{});
 
-    u32x4 kpre[CPT], vpre[CPT];
+    // Per-lane LDS read offsets (the tile and buffer offsets are immediates).
+    //   K operand: row 32kb + c, logical chunk 2kk + h.
+    uint32_t k_off[KSTEPS];
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-        kpre[i] = load16(rk, g_off[i]);
-        vpre[i] = load16(rv, g_off[i]);
-    }
-
-    // Per-lane LDS read offsets.
-    //   K operand: row 32kb + c, logical chunk 2kk + h -> slot (2kk + h) ^ (c & 7).
-    const uint32_t k_row_off = c * ROW_BYTES;
-    const int k_x = h ^ (c & 7);
+    for (int kk = 0; kk < KSTEPS; ++kk)
+        k_off[kk] = c * ROW_BYTES + (((2 * kk + h) ^ k_swizzle<D>(c)) * 16);
     //   V operand (transposing read, 16-lane groups): lane i = l%16 of group
-    //   gsel = (l%32)/16 addresses row base + 4h + i/4, columns 32db + 16gsel + 4(i%4).
+    //   gsel = (l%32)/16 addresses row 4h + i/4 of a 16-key chunk (the same
+    //   swizzle for all chunks and for the +8 rows) and columns
+    //   32db + 16gsel + 4(i%4), i.e. 32-byte segment 2db + gsel.
     const int li = lane & 15;
     const int gsel = (lane >> 4) & 1;
-    const uint32_t v_lane_off = (4 * h + (li >> 2)) * ROW_BYTES + 8 * (li & 3);
-    const int v_x = gsel ^ (li >> 2);
+    uint32_t v_off[DBLK];
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+        v_off[db] = (4 * h + (li >> 2)) * ROW_BYTES + 8 * (li & 3) +
+                    (((2 * db + gsel) ^ v_swizzle<D>(4 * h + (li >> 2))) * 32);
 
     f32x16 oacc[DBLK];
 #pragma unroll
     for (int db = 0; db < DBLK; ++db)
         for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
-    float m_run = -__builtin_inff();
-    float l_run = 0.0f;   // partial sum over this lane's keys
+    // Online-softmax state of this lane's query row.  m_ref is the reference
+    // maximum the exponents are taken against; it is raised (and O, l rescaled)
+    // only when a score exceeds it by more than 2^kLazy in the exp2 domain, so
+    // every probability stays <= 2^kLazy.  Any reference gives the same result
+    // in exact arithmetic, because O and l are divided by the same factor.
+    float m_ref = -__builtin_inff();
+    float mb = -__builtin_inff();   // m_ref * scale_log2
+    float l_run = 0.0f;             // partial sum over this lane's keys
     const float sl2 = p.scale_log2;
 
-    for (int n = 0; n < n_tiles; ++n) {
-        lds_char *const kb = lds + (n & 1) * 2 * TILE_BYTES;
+    auto tile_step = [&](const int n, auto buf) {
+        constexpr int BUF = decltype(buf)::value;
+        lds_char *const kb = lds + BUF * 2 * TILE_BYTES;
         lds_char *const vb = kb + TILE_BYTES;
-#pragma unroll
-        for (int i = 0; i < CPT; ++i) {
-            *(lds_u32x4 *)(kb + k_slot[i]) = kpre[i];
-            *(lds_u32x4 *)(vb + v_slot[i]) = vpre[i];
-        }
+        // This wave's copies of tile n have landed; after the barrier every
+        // wave's have, and every wave is done with tile n-1, whose buffer the
+        // copy of tile n+1 then overwrites while tile n is computed.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
-        if (n + 1 < n_tiles) {
-            const uint32_t next = (uint32_t)(n + 1) * TILE_BYTES;
-#pragma unroll
-            for (int i = 0; i < CPT; ++i) {
-                kpre[i] = load16(rk, next + g_off[i]);
-                vpre[i] = load16(rv, next + g_off[i]);
-            }
-        }
+        if (n + 1 < n_tiles) issue_tile(n + 1, Int<1 - BUF>{});
         const int key0 = n * BN;
-        if (CAUSAL && key0 > q_wave0 + 31) continue;   // every key after every row of this wave
+        if (CAUSAL && key0 > q_wave0 + 31) return;   // every key after every row of this wave
 
         // S^T = K Q^T
         f32x16 sacc[2];
@@ -201,8 +265,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         for (int kk = 0; kk < KSTEPS; ++kk) {
 #pragma unroll
             for (int kb2 = 0; kb2 < 2; ++kb2) {
-                const bf16x8 a = *(const lds_bf16x8 *)(kb + k_row_off + kb2 * 32 * ROW_BYTES +
-                                                       (((2 * kk) ^ k_x) * 16));
+                const bf16x8 a = *(const lds_bf16x8 *)(kb + k_off[kk] + kb2 * 32 * ROW_BYTES);
                 sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
             }
         }
@@ -220,31 +283,33 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
                 }
         }
 
-        // Online softmax: new running max, rescale factor, probabilities.
+        // Maximum over this lane's scores of the tile; the tile's first tile
+        // always holds key 0, so every row has a finite score there.
         float mx = sacc[0][0];
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb2][r]);
-        mx = fmaxf(mx, xor32(mx));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = exp2_hw((m_run - m_new) * sl2);
-        const float mb = m_new * sl2;
-        float lsum = 0.0f;
+        if (__any((mx - m_ref) * sl2 > kLazy)) {
+            // Raise the reference to the row maximum (both lane halves agree).
+            const float m_new = fmaxf(m_ref, fmaxf(mx, xor32(mx)));
+            const float alpha = exp2_hw((m_ref - m_new) * sl2);   // 0 on the first tile
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < DBLK; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+            m_ref = m_new;
+            mb = m_ref * sl2;
+        }
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const float pr = exp2_hw(__builtin_fmaf(sacc[kb2][r], sl2, -mb));
                 sacc[kb2][r] = pr;
-                lsum += pr;
+                l_run += pr;
             }
-        l_run = l_run * alpha + lsum;
-        m_run = m_new;
-#pragma unroll
-        for (int db = 0; db < DBLK; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
 
         // O^T += V^T P^T over four 16-key chunks.
 #pragma unroll
@@ -255,19 +320,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
 #pragma unroll
                 for (int e = 0; e < 8; ++e) p8[e] = sacc[kb2][8 * u + e];
                 const bf16x8 pb = __builtin_convertvector(p8, bf16x8);
-                const uint32_t chunk_off = (uint32_t)(16 * (2 * kb2 + u)) * ROW_BYTES + v_lane_off;
+                const int chunk = (16 * (2 * kb2 + u)) * ROW_BYTES;
 #pragma unroll
                 for (int db = 0; db < DBLK; ++db) {
-                    const uint32_t off = chunk_off + (((2 * db) ^ v_x) * 32);
                     const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                        (lds_bf16x4 *)(vb + off));
+                        (lds_bf16x4 *)(vb + v_off[db] + chunk));
                     const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                        (lds_bf16x4 *)(vb + off + 8 * ROW_BYTES));
+                        (lds_bf16x4 *)(vb + v_off[db] + chunk + 8 * ROW_BYTES));
                     const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
                     oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[db], 0, 0, 0);
                 }
             }
         }
+    };
+
+    // Two tiles per trip so that each LDS buffer has a fixed offset.
+    for (int n = 0; n < n_tiles; n += 2) {
+        tile_step(n, Int<0>{});
+        if (n + 1 < n_tiles) tile_step(n + 1, Int<1>{});
     }
 
     // O = acc / l, rounded to bf16; lane holds d = 32db + 8j + 4h + 0..3 of its row.
@@ -286,17 +356,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     }
 }
 
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, int MAPPING>
 hipError_t launch_one(const KernelArgs &a, int grid, hipStream_t stream) {
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL>), dim3(grid), dim3(kThreads), 0, stream, a);
+    if (a.heavy_first)
+        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, MAPPING, true>), dim3(grid), dim3(kThreads),
+                           0, stream, a);
+    else
+        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, MAPPING, false>), dim3(grid),
+                           dim3(kThreads), 0, stream, a);
     return hipGetLastError();
+}
+
+template <int D, bool CAUSAL>
+hipError_t launch_mapping(const KernelArgs &a, int mapping, int grid, hipStream_t stream) {
+    switch (mapping) {
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_one<D, CAUSAL, 0>(a, grid, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_one<D, CAUSAL, 1>(a, grid, stream);
+        default: return launch_one<D, CAUSAL, 2>(a, grid, stream);
+    }
 }
 
 }  // namespace
 
-hipError_t launch_attn_fwd(const KernelArgs &a, int d, bool causal, int grid, hipStream_t stream) {
-    if (d == 64) return causal ? launch_one<64, true>(a, grid, stream) : launch_one<64, false>(a, grid, stream);
-    return causal ? launch_one<128, true>(a, grid, stream) : launch_one<128, false>(a, grid, stream);
+hipError_t launch_attn_fwd(const KernelArgs &a, int d, bool causal, int mapping, int grid,
+                           hipStream_t stream) {
+    if (d == 64)
+        return causal ? launch_mapping<64, true>(a, mapping, grid, stream)
+                      : launch_mapping<64, false>(a, mapping, grid, stream);
+    return causal ? launch_mapping<128, true>(a, mapping, grid, stream)
+                  : launch_mapping<128, false>(a, mapping, grid, stream);
 }
 
 }  // namespace attn

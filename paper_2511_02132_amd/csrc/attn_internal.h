@@ -21,7 +21,7 @@ struct KernelArgs {
     int B, Hq, Hkv, Sq, Skv;
     int NB;           // ceil(Sq / kBlockM)
     int NX;           // XCD count used by the mapping
-    int mapping;      // ATTN_MAP_*
+    int heavy_first;  // ATTN_ORDER_HEAVY_FIRST was set
     float scale_log2; // scale * log2(e): softmax evaluated with exp2
 };
 
@@ -29,20 +29,26 @@ struct Tile {
     int b, hq, m;
 };
 
-// Workgroup id -> tile (b, hq, m) for mapping 0/1/2 (ATTN_MAP_*); integer only.
-// In the kernel the arguments are uniform, so this runs on the scalar unit.
+// Workgroup id -> tile (b, hq, m) for base mapping 0/1/2 (ATTN_MAP_*);
+// integer only.  In the kernel the arguments are uniform, so this runs on the
+// scalar unit.
 //   0 naive block-first:   digits of wid over (B, NB, Hq), heads fastest
 //   1 naive head-first:    digits of wid over (B, Hq, NB), blocks fastest
 //   2 swizzled head-first: digits over (B, Hq, NB) of the rank of wid in the
 //     XCD-major listing of the grid (XCD x = wid mod NX receives its k-th WG
 //     as wid = x + k*NX; the first N mod NX XCDs hold one WG more).
-__host__ __device__ inline Tile map_wid(int mapping, int wid, int B, int Hq, int NB, int NX) {
+// heavy_first (ATTN_ORDER_HEAVY_FIRST) then replaces m by NB-1-m: the XCD of
+// every (b, hq) is unchanged, but each head's row blocks are dispatched from
+// the last (under a causal mask the most expensive) to the first.
+__host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, int B, int Hq,
+                                        int NB, int NX) {
     Tile t;
     if (mapping == 0) {
         t.hq = wid % Hq;
         const int rest = wid / Hq;
         t.m = rest % NB;
         t.b = rest / NB;
+        if (heavy_first) t.m = NB - 1 - t.m;
         return t;
     }
     int L = wid;
@@ -58,10 +64,13 @@ __host__ __device__ inline Tile map_wid(int mapping, int wid, int B, int Hq, int
     const int rest = L / NB;
     t.hq = rest % Hq;
     t.b = rest / Hq;
+    if (heavy_first) t.m = NB - 1 - t.m;
     return t;
 }
 
-// Enqueue the forward kernel for head dimension d (64 or 128).
-hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int grid, hipStream_t stream);
+// Enqueue the forward kernel for head dimension d (64 or 128) and base mapping
+// 0/1/2 (one kernel instantiation per combination).
+hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int mapping, int grid,
+                           hipStream_t stream);
 
 }  // namespace attn

@@ -1,0 +1,217 @@
+"""Summarise rocprofv3 counter passes of ``bench.py --profile`` into profiles/.
+
+Each pass directory holds one rocprofv3 run (``-d DIR -o run -f csv json``) of
+
+    rocprofv3 --pmc <counters> -d DIR -o run -f csv json -- python3 bench.py --profile --workload W
+
+Every (mapping, block order) of the attention kernel is its own kernel symbol
+(``attn_fwd_kernel<d, causal, mapping, heavy_first>``), so one run per pass
+covers all variants.  The run also holds a one-workgroup launch (it can only
+run on XCD 0) and a 256 MiB device copy, used to attribute counter instances
+to XCDs and to scale FETCH_SIZE / WRITE_SIZE to bytes.
+
+    python -m paper_2511_02132_amd.rocprof_counters --workload W --out FILE.md \\
+        --cmd "<pass commands>" DIR_A DIR_B ...
+
+The summary ends with a ```json block that bench.py reads (only when its
+kernel_source_sha256 matches the current kernel sources).
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import json
+import os
+import re
+import sys
+from collections import defaultdict
+
+MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first"]
+KERNEL_RE = re.compile(r"attn_fwd_kernel<(\d+), (true|false), (\d), (true|false)>")
+
+
+def variant_of(kernel_name: str):
+    m = KERNEL_RE.search(kernel_name)
+    if not m:
+        return None
+    name = MAPPING_NAMES[int(m.group(3))]
+    return name + ("+heavy_first" if m.group(4) == "true" else "")
+
+
+def read_csv(d: str):
+    """rows of run_counter_collection.csv: (dispatch, kernel, grid, counter, value)."""
+    path = os.path.join(d, "run_counter_collection.csv")
+    out = []
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            out.append((int(row["Dispatch_Id"]), row["Kernel_Name"], int(row["Grid_Size"]),
+                        row["Counter_Name"], float(row["Counter_Value"])))
+    return out
+
+
+def per_xcc(d: str, counters=("TCC_HIT", "TCC_MISS")):
+    """{dispatch_id: {counter: [sum over the instances of XCC x for x in 0..7]}} from the JSON.
+
+    Records of a dispatch carry only the counter id; they are taken in the
+    order of that counter's instance list, whose dimension indices give the
+    XCC.  The one-workgroup launch checks this attribution."""
+    path = os.path.join(d, "run_results.json")
+    if not os.path.exists(path):
+        return {}
+    root = json.load(open(path))["rocprofiler-sdk-tool"][0]
+    inst = {}
+    names = {}
+    for c in root["counters"]:
+        cid = c["id"]["handle"]
+        names[cid] = c["name"]
+        xcc = []
+        for i in c["instances"]:
+            dims = {x["dimension_name"]: x["index"] for x in i["dimensions"]}
+            xcc.append(dims.get("DIMENSION_XCC", 0))
+        inst[cid] = xcc
+    out = {}
+    for rec in root["callback_records"]["counter_collection"]:
+        did = rec["dispatch_data"]["dispatch_info"]["dispatch_id"]
+        pos = defaultdict(int)
+        sums = defaultdict(lambda: [0.0] * 8)
+        for r in rec["records"]:
+            cid = r["counter_id"]["handle"]
+            k = pos[cid]
+            pos[cid] += 1
+            if names.get(cid) in counters and k < len(inst[cid]):
+                sums[names[cid]][inst[cid][k]] += r["value"]
+        out[did] = dict(sums)
+    return out
+
+
+def summarise(dirs, workload: str):
+    per_variant = defaultdict(lambda: defaultdict(list))
+    copy = defaultdict(list)
+    one_wg_dispatches = []
+    xcc_tables = {}
+    for d in dirs:
+        rows = read_csv(d)
+        for did, kname, grid, cname, val in rows:
+            v = variant_of(kname)
+            if v is not None and grid == 256:
+                one_wg_dispatches.append((d, did))
+                continue
+            if v is not None:
+                per_variant[v][cname].append((d, did, val))
+            elif "copy" in kname.lower():
+                copy[cname].append(val)
+        xcc_tables[d] = per_xcc(d)
+
+    def mean(vals):
+        return sum(vals) / len(vals) if vals else None
+
+    copy_bytes = 256 * 2 ** 20
+    fetch_fac = write_fac = None
+    if copy.get("FETCH_SIZE"):
+        fetch_fac = copy_bytes / (mean(copy["FETCH_SIZE"]) * 1024)
+    if copy.get("WRITE_SIZE"):
+        write_fac = copy_bytes / (mean(copy["WRITE_SIZE"]) * 1024)
+
+    # XCC attribution check on the one-workgroup launch
+    xcc0_share = None
+    for d, did in one_wg_dispatches:
+        t = xcc_tables.get(d, {}).get(did)
+        if t and "TCC_HIT" in t:
+            tot = [t["TCC_HIT"][x] + t.get("TCC_MISS", [0] * 8)[x] for x in range(8)]
+            if sum(tot) > 0:
+                xcc0_share = tot[0] / sum(tot)
+
+    result = {}
+    for v, cs in sorted(per_variant.items()):
+        ent = {}
+        vals = {c: mean([x[2] for x in lst]) for c, lst in cs.items()}
+        if "TCC_HIT" in vals and "TCC_MISS" in vals:
+            ent["l2_hit_rate"] = round(vals["TCC_HIT"] / (vals["TCC_HIT"] + vals["TCC_MISS"]), 4)
+            xs = []
+            for (d, did, _) in cs["TCC_HIT"]:
+                t = xcc_tables.get(d, {}).get(did)
+                if t and "TCC_HIT" in t and "TCC_MISS" in t:
+                    xs.append([t["TCC_HIT"][x] / max(1.0, t["TCC_HIT"][x] + t["TCC_MISS"][x])
+                               for x in range(8)])
+            if xs:
+                ent["l2_hit_rate_per_xcd"] = [round(sum(col) / len(col), 4) for col in zip(*xs)]
+        for c in ("TCC_HIT", "TCC_MISS", "TCC_EA0_RDREQ", "TCC_EA0_RDREQ_32B",
+                  "TCC_EA0_RDREQ_DRAM", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS",
+                  "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VALU",
+                  "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"):
+            if c in vals:
+                ent[c.lower()] = vals[c]
+        if "MfmaUtil" in vals:
+            ent["mfma_util_pct"] = round(vals["MfmaUtil"], 2)
+        if "FETCH_SIZE" in vals:
+            ent["fetch_kib"] = vals["FETCH_SIZE"]
+        if "WRITE_SIZE" in vals:
+            ent["write_kib"] = vals["WRITE_SIZE"]
+        if fetch_fac and write_fac and "FETCH_SIZE" in vals and "WRITE_SIZE" in vals:
+            ent["hbm_bytes_per_launch"] = int(vals["FETCH_SIZE"] * 1024 * fetch_fac +
+                                              vals["WRITE_SIZE"] * 1024 * write_fac)
+        result[v] = ent
+    return result, fetch_fac, write_fac, xcc0_share
+
+
+def compulsory_bytes(workload: str) -> int:
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import attn_inputs as ai
+    w = ai.WORKLOADS[workload]
+    qo = 2 * w["B"] * w["Hq"] * w["Sq"] * w["d"] * 2
+    kv = 2 * w["B"] * w["Hkv"] * w["Skv"] * w["d"] * 2
+    return qo + kv
+
+
+def write_md(out: str, workload: str, cmd: str, result, fetch_fac, write_fac, xcc0_share):
+    from paper_2511_02132_amd.build import kernel_source_hash
+
+    comp = compulsory_bytes(workload)
+    lines = ["# attn_fwd counters: %s" % workload, "",
+             "rocprofv3 counter passes over `bench.py --profile` (2 launches per variant; "
+             "values are per launch, averaged).", "",
+             "Commands (from the repository root on the GPU box; `cd /tmp` first, "
+             "paths absolute in the run):", "", "```", cmd.strip(), "```", "",
+             "Compulsory HBM bytes (Q, K, V read once, O written once): %d (%.1f MiB)."
+             % (comp, comp / 2 ** 20), ""]
+    if fetch_fac:
+        lines.append("Copy-kernel scale factors (256 MiB device copy): FETCH_SIZE x%.4f, "
+                     "WRITE_SIZE x%.4f." % (fetch_fac, write_fac or float('nan')))
+    if xcc0_share is not None:
+        lines.append("XCD attribution check: %.4f of the one-workgroup launch's L2 requests "
+                     "land on XCD 0 instances." % xcc0_share)
+    lines += ["", "| variant | L2 hit | L2 hit per XCD (min..max) | HBM bytes / launch | "
+                  "/ compulsory | MFMA util % | LDS bank-conflict cycles |",
+              "|---|---|---|---|---|---|---|"]
+    for v, e in result.items():
+        px = e.get("l2_hit_rate_per_xcd")
+        hb = e.get("hbm_bytes_per_launch")
+        lines.append("| %s | %s | %s | %s | %s | %s | %s |" % (
+            v, "%.1f%%" % (100 * e["l2_hit_rate"]) if "l2_hit_rate" in e else "-",
+            "%.1f..%.1f%%" % (100 * min(px), 100 * max(px)) if px else "-",
+            "%.3e" % hb if hb else "-", "%.2f" % (hb / comp) if hb else "-",
+            e.get("mfma_util_pct", "-"), "%.3e" % e["sq_lds_bank_conflict"]
+            if "sq_lds_bank_conflict" in e else "-"))
+    data = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
+            "compulsory_bytes": comp, "fetch_scale": fetch_fac, "write_scale": write_fac,
+            "xcc0_share_one_wg": xcc0_share, "per_mapping": result}
+    lines += ["", "```json", json.dumps(data, indent=1, sort_keys=True), "```", ""]
+    with open(out, "w") as f:
+        f.write("\n".join(lines))
+
+
+def main(argv=None):
+    p = argparse.ArgumentParser()
+    p.add_argument("--workload", required=True)
+    p.add_argument("--out", required=True)
+    p.add_argument("--cmd", default="", help="the commands that produced the passes")
+    p.add_argument("dirs", nargs="+")
+    a = p.parse_args(argv)
+    res = summarise(a.dirs, a.workload)
+    write_md(a.out, a.workload, a.cmd, *res)
+    print(open(a.out).read())
+
+
+if __name__ == "__main__":
+    main()

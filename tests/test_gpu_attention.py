@@ -20,6 +20,9 @@ from oracle import mapping as mp
 
 pytestmark = pytest.mark.gpu
 
+# the three mappings, each with the paper's block order and with heavy-first order
+ALL_MAPPINGS = [m | f for m in (0, 1, 2) for f in (0, 0x10)]
+
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
 DEV = "cuda:0"
@@ -65,11 +68,12 @@ def test_probe_matches_enumeration_and_dispatch(B, Hq, Hkv, S, d):
     nx = pa.num_xcd()
     BM = pa.block_m(d)
     outs = []
-    for mapping in mp.MAPPINGS:
-        o, probe = pa.attn_fwd_probe(q, k, v, causal=True, mapping=mapping)
+    for mapping, heavy in [(m, hf) for m in mp.MAPPINGS for hf in (False, True)]:
+        flag = pa.HEAVY_FIRST if heavy else 0
+        o, probe = pa.attn_fwd_probe(q, k, v, causal=True, mapping=mapping | flag)
         torch.cuda.synchronize()
         rec = probe.cpu().numpy()
-        want = mp.enumerate_mapping(mapping, B, Hq, S, BM, nx)
+        want = mp.enumerate_mapping(mapping, B, Hq, S, BM, nx, heavy_first=heavy)
         assert np.array_equal(rec[:, :3], want), "placement differs from the enumeration"
         wid = np.arange(rec.shape[0])
         assert np.array_equal(rec[:, 3], wid % nx), "XCC_ID != wid mod NX"
@@ -109,7 +113,7 @@ def test_parity_small(B, Hq, Hkv, Sq, Skv, d, causal):
     scale = ai.default_scale(d)
     ref = oracle.attn_fwd_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), causal, scale)
     qd, kd, vd = _to_dev(q, k, v)
-    outs = [_run(qd, kd, vd, causal, scale, m) for m in mp.MAPPINGS]
+    outs = [_run(qd, kd, vd, causal, scale, m) for m in ALL_MAPPINGS]
     for o in outs:
         assert not torch.isnan(o).any(), "unwritten output elements"
         mx, mean = _err(o, ref)
@@ -189,7 +193,7 @@ def test_parity_full_size_sampled_rows(name):
     scale = ai.default_scale(w["d"])
     causal = w["causal"]
     qd, kd, vd = _to_dev(q, k, v)
-    outs = [_run(qd, kd, vd, causal, scale, m) for m in mp.MAPPINGS]
+    outs = [_run(qd, kd, vd, causal, scale, m) for m in ALL_MAPPINGS]
     for o in outs:
         assert not torch.isnan(o).any(), "unwritten output elements"
     for o in outs[1:]:

@@ -128,7 +128,26 @@ def pin_ceil_blocks(m):
     assert m.num_row_blocks(1, 128) == 1 and m.grid_size(2, 3, 129, 128) == 12
 
 
-PINS = [pin_permutation, pin_chiplet_swizzle, pin_head_first_listing, pin_caption_example,
+def pin_heavy_first_order(m):
+    """The order option keeps each (b, hq) on its XCD and reverses each head's block order."""
+    for (B, Hq, NB, NX) in SHAPES[::7]:
+        for mapping in mp.MAPPINGS:
+            N = B * Hq * NB
+            base = [m.map_wid(mapping, w, B, Hq, NB, NX) for w in range(N)]
+            rev = [m.map_wid(mapping, w, B, Hq, NB, NX, True) for w in range(N)]
+            assert sorted(rev) == sorted(base)
+            for w in range(N):
+                assert rev[w][:2] == base[w][:2] and rev[w][2] == NB - 1 - base[w][2]
+    # swizzled head-first: each XCD sees every head's blocks in decreasing order
+    B, Hq, NB, NX = 1, 16, 12, 8
+    seen = {}
+    for w in range(B * Hq * NB):
+        b, h, blk = m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, True)
+        seen.setdefault((w % NX, h), []).append(blk)
+    assert all(v == sorted(v, reverse=True) and len(v) == NB for v in seen.values())
+
+
+PINS = [pin_heavy_first_order, pin_permutation, pin_chiplet_swizzle, pin_head_first_listing, pin_caption_example,
         pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_ceil_blocks]
 
 
@@ -162,18 +181,22 @@ class _Mutant:
         # map_wid must see the replaced helpers
         me = self
 
-        def map_wid(mapping, wid, B, Hq, NB, NX):
+        def map_wid(mapping, wid, B, Hq, NB, NX, heavy_first=False):
             N = B * Hq * NB
             if not 0 <= wid < N:
                 raise ValueError("wid out of range")
             if mapping == mp.NAIVE_BLOCK_FIRST:
                 b, mm, hq = me.unravel(wid, me.bf_radices(B, Hq, NB))
-                return b, hq, mm
-            if mapping == mp.NAIVE_HEAD_FIRST:
-                return me.unravel(wid, (B, Hq, NB))
-            return me.unravel(me.swizzled_rank(wid, N, NX), (B, Hq, NB))
+            elif mapping == mp.NAIVE_HEAD_FIRST:
+                b, hq, mm = me.unravel(wid, (B, Hq, NB))
+            else:
+                b, hq, mm = me.unravel(me.swizzled_rank(wid, N, NX), (B, Hq, NB))
+            if heavy_first:
+                mm = me.reverse_block(mm, NB)
+            return b, hq, mm
         self.map_wid = overrides.get("map_wid", map_wid)
         self.__dict__.setdefault("bf_radices", lambda B, Hq, NB: (B, NB, Hq))
+        self.__dict__.setdefault("reverse_block", lambda mm, NB: NB - 1 - mm)
 
 
 def _unravel_first_fastest(x, radices):
@@ -200,6 +223,7 @@ MAP_MUTANTS = {
     "swizzle_identity": dict(swizzled_rank=lambda wid, N, NX: wid),
     "block_first_head_outer": dict(bf_radices=lambda B, Hq, NB: (B, Hq, NB)),
     "floor_row_blocks": dict(num_row_blocks=lambda Sq, BM: Sq // BM),
+    "heavy_first_off_by_one": dict(reverse_block=lambda mm, NB: (NB - mm) % NB),
 }
 
 
