@@ -201,15 +201,50 @@ def write_md(out: str, workload: str, cmd: str, result, fetch_fac, write_fac, xc
         f.write("\n".join(lines))
 
 
+def write_stats_md(out: str, stats_csv: str, bench_json: str, cmd: str):
+    """Kernel-trace statistics of a bench.py run next to the bench line it printed."""
+    from paper_2511_02132_amd.build import kernel_source_hash
+
+    rows = list(csv.DictReader(open(stats_csv)))
+    line = open(bench_json).read().strip().splitlines()[-1]
+    bench = json.loads(line)
+    head = bench["config"]["mapping"]
+    lines = ["# attn_fwd kernel trace: %s" % bench["config"]["workload"], "",
+             "Command (repository root on the GPU box; `cd /tmp` first, paths absolute):", "",
+             "```", cmd.strip(), "```", "",
+             "Kernel source sha256[:16]: `%s`" % kernel_source_hash(), "",
+             "| kernel | calls | average us | min us | max us | share |",
+             "|---|---|---|---|---|---|"]
+    for r in rows:
+        v = variant_of(r["Name"]) or r["Name"][:60]
+        lines.append("| %s | %s | %.1f | %.1f | %.1f | %s%% |" % (
+            v, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+            float(r["MaxNs"]) / 1e3, r["Percentage"]))
+    avg = [float(r["AverageNs"]) / 1e3 for r in rows if variant_of(r["Name"]) == head]
+    lines += ["", "Headline variant `%s`: bench.py timed %.1f us per step with HIP events on the "
+              "launch stream (its K back-to-back steps); the profiler's average over all "
+              "calls of that kernel (warm-up, timed steps and the cold/warm per-mapping reps) "
+              "is %s us." % (head, bench["ms_per_step"] * 1e3,
+                             "%.1f" % avg[0] if avg else "n/a"),
+              "", "bench.py line printed under the profiler:", "", "```json", line, "```", ""]
+    with open(out, "w") as f:
+        f.write("\n".join(lines))
+
+
 def main(argv=None):
     p = argparse.ArgumentParser()
-    p.add_argument("--workload", required=True)
+    p.add_argument("--workload")
     p.add_argument("--out", required=True)
     p.add_argument("--cmd", default="", help="the commands that produced the passes")
-    p.add_argument("dirs", nargs="+")
+    p.add_argument("--stats-csv", help="kernel_stats.csv of a --kernel-trace --stats run")
+    p.add_argument("--bench-json", help="the bench.py output of that run")
+    p.add_argument("dirs", nargs="*")
     a = p.parse_args(argv)
-    res = summarise(a.dirs, a.workload)
-    write_md(a.out, a.workload, a.cmd, *res)
+    if a.stats_csv:
+        write_stats_md(a.out, a.stats_csv, a.bench_json, a.cmd)
+    else:
+        res = summarise(a.dirs, a.workload)
+        write_md(a.out, a.workload, a.cmd, *res)
     print(open(a.out).read())
 
 
