@@ -15,11 +15,11 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libattn_numa.so")
-SOURCES = ["attn_fwd.hip", "attn_abi.cpp"]
+SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_abi.cpp"]
 ARCH = "gfx950"
 
 
-KERNEL_SOURCES = ["attn_fwd.hip", "attn_internal.h"]
+KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_device.h", "attn_internal.h"]
 
 
 def kernel_source_hash() -> str:
@@ -57,6 +57,12 @@ def build(out: str = LIB, verbose: bool = False) -> str:
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed building %s" % out)
+    # Surface warnings, except the host pass's note that it does not know the
+    # device-only packed-fp32 feature.
+    noise = ("packed-fp32-ops' is not a recognized feature",)
+    for line in (res.stdout + res.stderr).splitlines():
+        if line.strip() and not any(n in line for n in noise):
+            sys.stderr.write(line + "\n")
     os.replace(tmp, out)
     return out
 

@@ -36,9 +36,10 @@ int check_shape(int B, int Hq, int Hkv, int Sq, int Skv, int d) {
     if (Hq % Hkv != 0) return ATTN_ERR_SHAPE;
     if (!supported_d(d)) return ATTN_ERR_UNSUPPORTED;
     const int64_t lim = INT32_MAX;
-    if (((int64_t)Sq + attn::kBlockM) * d * 2 > lim) return ATTN_ERR_SHAPE;
-    if (((int64_t)Skv + attn::kBlockN) * d * 2 > lim) return ATTN_ERR_SHAPE;
-    const int64_t nb = ((int64_t)Sq + attn::kBlockM - 1) / attn::kBlockM;
+    if (((int64_t)Sq + attn::kMaxBlockM) * d * 2 > lim) return ATTN_ERR_SHAPE;
+    if (((int64_t)Skv + 2 * attn::kBlockN) * d * 2 > lim) return ATTN_ERR_SHAPE;
+    const int bm = attn::block_m_for(d);
+    const int64_t nb = ((int64_t)Sq + bm - 1) / bm;
     if ((int64_t)B * Hq * nb > lim) return ATTN_ERR_SHAPE;
     return ATTN_OK;
 }
@@ -98,7 +99,7 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.Hkv = Hkv;
     a.Sq = Sq;
     a.Skv = Skv;
-    a.NB = (Sq + attn::kBlockM - 1) / attn::kBlockM;
+    a.NB = (Sq + attn::block_m_for(d) - 1) / attn::block_m_for(d);
     a.NX = nx;
     a.heavy_first = (mapping & ATTN_ORDER_HEAVY_FIRST) != 0;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
@@ -127,7 +128,8 @@ int attn_fwd_probe(const void *q, const void *k, const void *v, void *o, int B, 
 int64_t attn_grid_size(int B, int Hq, int Sq, int d) {
     if (B <= 0 || Hq <= 0 || Sq <= 0 || d <= 0) return ATTN_ERR_SHAPE;
     if (!supported_d(d)) return ATTN_ERR_UNSUPPORTED;
-    return (int64_t)B * Hq * (((int64_t)Sq + attn::kBlockM - 1) / attn::kBlockM);
+    const int bm = attn::block_m_for(d);
+    return (int64_t)B * Hq * (((int64_t)Sq + bm - 1) / bm);
 }
 
 int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *out) {
@@ -137,7 +139,7 @@ int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *o
     const int64_t n = attn_grid_size(B, Hq, Sq, d);
     if (n < 0) return (int)n;
     if (n > INT32_MAX) return ATTN_ERR_SHAPE;
-    const int nb = (Sq + attn::kBlockM - 1) / attn::kBlockM;
+    const int nb = (Sq + attn::block_m_for(d) - 1) / attn::block_m_for(d);
     for (int64_t wid = 0; wid < n; ++wid) {
         const attn::Tile t = attn::map_wid(mapping & 0xf, (mapping & ATTN_ORDER_HEAVY_FIRST) != 0,
                                            (int)wid, B, Hq, nb, NX);
@@ -148,7 +150,7 @@ int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *o
     return ATTN_OK;
 }
 
-int attn_block_m(int d) { return supported_d(d) ? attn::kBlockM : ATTN_ERR_UNSUPPORTED; }
+int attn_block_m(int d) { return supported_d(d) ? attn::block_m_for(d) : ATTN_ERR_UNSUPPORTED; }
 
 int attn_block_n(int d) { return supported_d(d) ? attn::kBlockN : ATTN_ERR_UNSUPPORTED; }
 

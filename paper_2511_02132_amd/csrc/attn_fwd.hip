@@ -43,91 +43,14 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "attn_numa.h"
+#include "attn_device.h"
 #include "attn_internal.h"
+#include "attn_numa.h"
 
 namespace attn {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-
-typedef __attribute__((address_space(3))) char lds_char;
-typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
-typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
-
-constexpr int kThreads = 256;
-// Word 3 of a gfx9 buffer resource: 32-bit data format, raw (stride 0) access.
-constexpr int kBufferFlags = 0x00020000;
-
-// Buffer resource as four scalar words (gfx9 layout): base address, stride 0,
-// size in bytes (accesses at or past it read zero / are dropped), flags.
-__device__ __forceinline__ i32x4 buffer_words(const void *base, uint32_t bytes) {
-    const uint64_t a = (uint64_t)base;
-    i32x4 r;
-    r[0] = (int)(uint32_t)a;
-    r[1] = (int)(uint32_t)(a >> 32) & 0xffff;
-    r[2] = (int)bytes;
-    r[3] = kBufferFlags;
-    return r;
-}
-
-// 16 bytes per lane from global memory straight into LDS: lane j's bytes land
-// at lds_addr + 16*j.  Issued from inline assembly so that the compiler does
-// not order later LDS reads of the other buffer behind it; the kernel waits for
-// these copies itself (vmcnt) before the barrier that publishes a tile.
-__device__ __forceinline__ void lds_copy16(i32x4 rsrc, uint32_t voffset, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :
-                 : "v"(voffset), "s"(rsrc), "s"(lds_addr)
-                 : "memory", "m0");
-}
-
-__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t rsrc, uint32_t byte_off) {
-    return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)byte_off, 0, 0);
-}
-
-__device__ __forceinline__ float xor32(float x) {
-    // value held by lane l ^ 32
-    return __shfl_xor(x, 32, 64);
-}
-
-__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// s_waitcnt operand: vmcnt(0), expcnt and lgkmcnt not waited for.
-constexpr int kWaitVmcnt0 = 0x0f70;
-
-// LDS swizzles.  gfx950 serves 16 lanes of a 16-byte read (or of the 8-byte
-// transposing read) from 64 four-byte banks, a 256-byte window; sixteen
-// consecutive rows must therefore land in sixteen distinct 16-byte bank groups.
-//   K rows (read as 16-byte chunks by 16 consecutive rows): chunk c of row r is
-//   stored at c ^ k_swizzle(r); for 128-byte rows two rows share a window.
-template <int D>
-__device__ __forceinline__ int k_swizzle(int row) {
-    return D == 128 ? (row & 15) : ((row >> 1) & 7);
-}
-//   V rows (read 4 rows x 32 bytes per 16 lanes, two such groups on adjacent
-//   segments per 32 lanes): 32-byte segment s of row r is stored at
-//   s ^ v_swizzle(r), which keeps all 8 (row, segment) pairs of 32 lanes apart.
-template <int D>
-__device__ __forceinline__ int v_swizzle(int row) {
-    return D == 128 ? 2 * (row & 3) : 2 * ((row >> 1) & 1);
-}
-
-template <int V>
-struct Int {
-    static constexpr int value = V;
-};
-
-// Lazy rescaling threshold (exp2 domain): probabilities stay below 2^8.
-constexpr float kLazy = 8.0f;
+using namespace dev;
 
 template <int D, bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs p) {
@@ -183,6 +106,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     // 16 bytes at j*16, so the swizzled layout is made by choosing which
     // global 16-byte chunk each lane fetches.  Wave w fills LDS slots
     // (w*IPW + i)*64 + lane, i < IPW, of each tile.
+    //
+    // LDS holds two K buffers and two V buffers.  The K stream runs one tile
+    // ahead of the V stream: while tile n's probabilities are formed and
+    // multiplied into V(n), the scores of tile n+1 are already being computed
+    // from K(n+1).  At the top of iteration n, K(n+1) and V(n) have landed and
+    // every wave is done with K(n) and V(n-1), whose buffers then receive
+    // K(n+2) and V(n+1).
     uint32_t k_src[IPW], v_src[IPW];
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
@@ -193,25 +123,27 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         const int seg = (phys >> 1) ^ v_swizzle<D>(row);
         v_src[i] = row * ROW_BYTES + (seg * 2 + (phys & 1)) * 16;
     }
-    const i32x4 wk = buffer_words((const char *)p.k + kv_head * 2, p.Skv * ROW_BYTES);
-    const i32x4 wv = buffer_words((const char *)p.v + kv_head * 2, p.Skv * ROW_BYTES);
+    const char *const k_head = (const char *)p.k + kv_head * 2;
+    const char *const v_head = (const char *)p.v + kv_head * 2;
+    const uint32_t kv_bytes = p.Skv * ROW_BYTES;
     const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
-    auto issue_tile = [&](const int n, auto buf) {
-        constexpr int BUF = decltype(buf)::value;
-        const uint32_t tile = (uint32_t)n * TILE_BYTES;
+    // Copy of tile n of K (or V) into LDS buffer `buf`; the descriptor starts
+    // at the tile, so the per-lane offsets stay fixed.
+    auto copy_tile = [&](const char *head, const uint32_t *src, const int n, const int buf) __attribute__((always_inline)) {
+        const uint32_t off = (uint32_t)n * TILE_BYTES;
+        const i32x4 d = buffer_words(head + off, kv_bytes - off);
 #pragma unroll
-        for (int i = 0; i < IPW; ++i) {
-            const uint32_t dst = lds_base + BUF * 2 * TILE_BYTES + (w * IPW + i) * 1024;
-            lds_copy16(wk, tile + k_src[i], dst);
-            lds_copy16(wv, tile + v_src[i], dst + TILE_BYTES);
-        }
+        for (int i = 0; i < IPW; ++i)
+            lds_copy16(d, src[i], lds_base + buf * TILE_BYTES + (w * IPW + i) * 1024);
     };
+    // buffers: K0, K1, V0, V1
+    auto copy_k = [&](const int n, const int kbuf) __attribute__((always_inline)) { copy_tile(k_head, k_src, n, kbuf); };
+    auto copy_v = [&](const int n, const int vbuf) __attribute__((always_inline)) { copy_tile(v_head, v_src, n, 2 + vbuf); };
 
     const int kv_end = CAUSAL ? min((t.m + 1) * BM, p.Skv) : p.Skv;
     const int n_tiles = (kv_end + BN - 1) / BN;
-    issue_tile(0, Int<0>{});
 
-    // Per-lane LDS read offsets (the tile and buffer offsets are immediates).
+    // Per-lane LDS read offsets (the buffer offsets are immediates).
     //   K operand: row 32kb + c, logical chunk 2kk + h.
     uint32_t k_off[KSTEPS];
 #pragma unroll
@@ -229,6 +161,22 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         v_off[db] = (4 * h + (li >> 2)) * ROW_BYTES + 8 * (li & 3) +
                     (((2 * db + gsel) ^ v_swizzle<D>(4 * h + (li >> 2))) * 32);
 
+    // S^T of one tile from K buffer `kbuf`.
+    auto scores = [&](const int kbuf, f32x16 (&sacc)[2]) {
+        lds_char *const kb = lds + kbuf * TILE_BYTES;
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+            for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk) {
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2) {
+                const bf16x8 a = *(const lds_bf16x8 *)(kb + k_off[kk] + kb2 * 32 * ROW_BYTES);
+                sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
+            }
+        }
+    };
+
     f32x16 oacc[DBLK];
 #pragma unroll
     for (int db = 0; db < DBLK; ++db)
@@ -243,33 +191,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     float l_run = 0.0f;             // partial sum over this lane's keys
     const float sl2 = p.scale_log2;
 
-    auto tile_step = [&](const int n, auto buf) {
-        constexpr int BUF = decltype(buf)::value;
-        lds_char *const kb = lds + BUF * 2 * TILE_BYTES;
-        lds_char *const vb = kb + TILE_BYTES;
-        // This wave's copies of tile n have landed; after the barrier every
-        // wave's have, and every wave is done with tile n-1, whose buffer the
-        // copy of tile n+1 then overwrites while tile n is computed.
+    // Prologue: K(0), V(0), K(1) in flight; scores of tile 0.
+    copy_k(0, 0);
+    copy_v(0, 0);
+    if (n_tiles > 1) copy_k(1, 1);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    f32x16 s_cur[2];
+    scores(0, s_cur);
+
+    // Iteration n (buffers fixed by the parity of n): softmax and P V of tile
+    // n, scores of tile n+1.
+    auto tile_step = [&](const int n, auto parity) __attribute__((always_inline)) {
+        constexpr int PAR = decltype(parity)::value;   // n % 2
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
-        if (n + 1 < n_tiles) issue_tile(n + 1, Int<1 - BUF>{});
+        if (n + 2 < n_tiles) copy_k(n + 2, PAR);
+        if (n + 1 < n_tiles) copy_v(n + 1, 1 - PAR);
+
         const int key0 = n * BN;
-        if (CAUSAL && key0 > q_wave0 + 31) return;   // every key after every row of this wave
-
-        // S^T = K Q^T
-        f32x16 sacc[2];
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-            for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.0f;
-#pragma unroll
-        for (int kk = 0; kk < KSTEPS; ++kk) {
-#pragma unroll
-            for (int kb2 = 0; kb2 < 2; ++kb2) {
-                const bf16x8 a = *(const lds_bf16x8 *)(kb + k_off[kk] + kb2 * 32 * ROW_BYTES);
-                sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
-            }
-        }
-
         // Mask keys past Skv and, when causal, keys after the query row.
         const bool need_mask = (key0 + BN > p.Skv) || (CAUSAL && key0 + BN - 1 > q_wave0);
         if (need_mask) {
@@ -279,17 +219,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
                 for (int r = 0; r < 16; ++r) {
                     const int key = key0 + 32 * kb2 + 8 * (r >> 2) + 4 * h + (r & 3);
                     const bool dead = key >= p.Skv || (CAUSAL && key > my_q);
-                    sacc[kb2][r] = dead ? -__builtin_inff() : sacc[kb2][r];
+                    s_cur[kb2][r] = dead ? -__builtin_inff() : s_cur[kb2][r];
                 }
         }
-
-        // Maximum over this lane's scores of the tile; the tile's first tile
-        // always holds key 0, so every row has a finite score there.
-        float mx = sacc[0][0];
+        // Maximum over this lane's scores of the tile (tile 0 holds key 0, so
+        // every row has a finite score there).
+        float mx = s_cur[0][0];
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb2][r]);
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kb2][r]);
         if (__any((mx - m_ref) * sl2 > kLazy)) {
             // Raise the reference to the row maximum (both lane halves agree).
             const float m_new = fmaxf(m_ref, fmaxf(mx, xor32(mx)));
@@ -302,23 +241,27 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
             m_ref = m_new;
             mb = m_ref * sl2;
         }
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float pr = exp2_hw(__builtin_fmaf(sacc[kb2][r], sl2, -mb));
-                sacc[kb2][r] = pr;
-                l_run += pr;
-            }
 
-        // O^T += V^T P^T over four 16-key chunks.
+        // Scores of the next tile, independent of the work below so the two
+        // interleave.  After the last tile this reads a stale (in-bounds)
+        // buffer and the result is dropped; computing it unconditionally keeps
+        // the loop body one basic block.
+        f32x16 s_next[2];
+        scores(1 - PAR, s_next);
+
+        // Probabilities of tile n and O^T += V^T P^T over four 16-key chunks.
+        lds_char *const vb = lds + (2 + PAR) * TILE_BYTES;
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2) {
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 f32x8 p8;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) p8[e] = sacc[kb2][8 * u + e];
+                for (int e = 0; e < 8; ++e) {
+                    const float pr = exp2_hw(__builtin_fmaf(s_cur[kb2][8 * u + e], sl2, -mb));
+                    p8[e] = pr;
+                    l_run += pr;
+                }
                 const bf16x8 pb = __builtin_convertvector(p8, bf16x8);
                 const int chunk = (16 * (2 * kb2 + u)) * ROW_BYTES;
 #pragma unroll
@@ -332,6 +275,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
                 }
             }
         }
+        s_cur[0] = s_next[0];
+        s_cur[1] = s_next[1];
     };
 
     // Two tiles per trip so that each LDS buffer has a fixed offset.
@@ -380,11 +325,9 @@ hipError_t launch_mapping(const KernelArgs &a, int mapping, int grid, hipStream_
 
 hipError_t launch_attn_fwd(const KernelArgs &a, int d, bool causal, int mapping, int grid,
                            hipStream_t stream) {
-    if (d == 64)
-        return causal ? launch_mapping<64, true>(a, mapping, grid, stream)
-                      : launch_mapping<64, false>(a, mapping, grid, stream);
-    return causal ? launch_mapping<128, true>(a, mapping, grid, stream)
-                  : launch_mapping<128, false>(a, mapping, grid, stream);
+    if (d == 128) return launch_attn_fwd_d128(a, causal, mapping, grid, stream);
+    return causal ? launch_mapping<64, true>(a, mapping, grid, stream)
+                  : launch_mapping<64, false>(a, mapping, grid, stream);
 }
 
 }  // namespace attn

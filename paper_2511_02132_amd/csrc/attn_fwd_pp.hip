@@ -1,0 +1,468 @@
+// attn_fwd_pp.hip -- fused attention forward for gfx950, head dimension 128:
+// two wave groups that alternate matrix-core and vector work ("ping-pong").
+//
+// Same result as the 4-wave kernel of attn_fwd.hip (Section 2.3, Eq. "eq:fa",
+// with the FlashAttention-2 partition of Section 2.3.1 and the mappings of
+// Sections 3.2 and 3.3), organised so that the two contractions run on the
+// matrix cores while the softmax of another tile runs on the vector ALUs.
+//
+// Workgroup: 512 threads = 8 waves over BLOCK_M = 256 query rows.  Waves w and
+// w+4 share a SIMD (the hardware places them so; checked on MI355X), wave w
+// owns rows 32w..32w+31.  Group A = waves 0-3 (rows 0..127), group B = waves
+// 4-7 (rows 128..255); both stream the same K/V tiles of 64 keys.
+//
+// Per tile j a group does two steps:
+//   E(j): softmax of S(j): mask, lazy running max, P = exp2(...), P -> bf16
+//         (vector ALU);
+//   G(j): S(j+1) = K(j+1) Q^T, O^T += V(j)^T P(j)^T and the row sums of P(j)
+//         (36 MFMAs).
+// The groups run these one phase apart, phases separated by workgroup
+// barriers:
+//   phase 2k:   A: E(k)   B: G(k-1)
+//   phase 2k+1: A: G(k)   B: E(k)
+// so on every SIMD one wave feeds the matrix core while the other computes
+// exponentials.  Both groups execute the same instruction stream (E, G, E,
+// G, ...); only their first barrier differs.
+//
+// LDS: kStages stages of 32 KiB, stage j = {K(j+1), V(j)}, read in phases
+// 2j+1 (A) and 2j+2 (B) and copied global -> LDS (buffer_load ... lds) kAhead
+// stages ahead; optionally (kQInLds) the block's Q rows as well.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn_device.h"
+#include "attn_internal.h"
+#include "attn_numa.h"
+
+namespace attn {
+namespace {
+
+using namespace dev;
+
+constexpr int kPPThreads = 512;
+// LDS operand reads issued this many MFMAs ahead in the product step.
+constexpr int kPrefetch = 6;
+// Q operands in LDS (true) or in registers (false).
+constexpr bool kQInLds = false;
+// K/V stages resident in LDS, and how many stages ahead each copy is issued.
+constexpr int kStages = 2;
+constexpr int kAhead = 1;
+static_assert(kAhead >= 1 && kAhead < kStages, "a copy must not overwrite a stage in use");
+
+
+// Waits and the workgroup barrier.  The copies into LDS are invisible to the
+// compiler, so the waits are explicit; the barrier is a compiler memory fence
+// but does not wait for outstanding copies.
+// The scheduling barriers keep each step's instructions on its side of the
+// workgroup barrier, so that the phases stay separated.
+__device__ __forceinline__ void barrier_lds() {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+__device__ __forceinline__ void barrier_lds_copies() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+// Pin a value's computation before this point: without it the compiler sinks
+// the softmax arithmetic (and the MFMAs) next to their uses in the next step,
+// across the barrier, which would merge the two phases again.
+template <typename T>
+__device__ __forceinline__ void anchor(T &x) {
+    asm volatile("" : "+v"(x));
+}
+
+// Instruction-class masks of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
+
+// LDS reads feeding MFMA i of the product step: a K chunk (one 16-byte read)
+// for even i, a V column chunk (two transposing reads) for odd i.
+__host__ __device__ constexpr int a_reads(int i) { return (i & 1) ? 2 : 1; }
+
+// Scheduling groups of the product step (see gemm_step): the prologue reads,
+// then per MFMA i the reads for MFMA i+PF (and, before each even k-step, the
+// next Q operand) followed by MFMA i.
+__host__ __device__ constexpr int prologue_reads(int pf) {
+    int n = 1;   // Q operand of k-step 0
+    for (int i = 0; i < pf; ++i) n += a_reads(i);
+    return n;
+}
+__host__ __device__ constexpr int step_reads(int pf, int i) {
+    return (i + pf < 32 ? a_reads(i + pf) : 0) +
+           (((i & 1) == 0 && ((i >> 1) & 1) == 0 && (i >> 2) + 1 < 8) ? 1 : 0);
+}
+template <int PF, int I>
+__device__ __forceinline__ void gemm_schedule_step() {
+    if constexpr (I < 32) {
+        constexpr int n = step_reads(PF, I);
+        if constexpr (n > 0) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, n, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+        gemm_schedule_step<PF, I + 1>();
+    }
+}
+template <int PF>
+__device__ __forceinline__ void gemm_schedule_impl() {
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, prologue_reads(PF), 0);
+    gemm_schedule_step<PF, 0>();
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4, 0);
+}
+
+// Wait until at most 4*n copy instructions (the n newest stages) are in flight.
+__device__ __forceinline__ void wait_copies(const int n) {
+    if (n <= 0)
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if (n == 1)
+        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+}
+
+template <bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
+__global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const KernelArgs p) {
+    constexpr int D = 128;
+    constexpr int BM = kBlockM128;
+    constexpr int BN = kBlockN;
+    constexpr int KSTEPS = D / 16;
+    constexpr int DBLK = D / 32;
+    constexpr int CHUNKS_PER_ROW = D / 8;
+    constexpr int ROW_BYTES = D * 2;
+    constexpr int TILE_BYTES = BN * ROW_BYTES;
+    constexpr int STAGE_BYTES = 2 * TILE_BYTES;
+    constexpr int WAVES = kPPThreads / 64;
+    constexpr int IPW = TILE_BYTES / 1024 / WAVES;   // copy instructions per wave per tile
+    static_assert(IPW * 1024 * WAVES == TILE_BYTES, "tile not divisible");
+
+    constexpr int Q_BYTES = kQInLds ? BM * ROW_BYTES : 0;   // the block's Q rows, swizzled like K
+    __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE_BYTES + Q_BYTES];
+    lds_char *const lds = (lds_char *)smem;
+    lds_char *const q_lds = lds + kStages * STAGE_BYTES;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = w >> 2;
+    const int c = lane & 31;
+    const int h = lane >> 5;
+
+    const Tile t = map_wid(MAPPING, HEAVY_FIRST, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
+    if (p.probe != nullptr && tid == 0) {
+        unsigned xcc;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+        int32_t *rec = p.probe + 4 * (int64_t)blockIdx.x;
+        rec[0] = t.b;
+        rec[1] = t.hq;
+        rec[2] = t.m;
+        rec[3] = (int)(xcc & 0xf);
+    }
+    const int g = t.hq / (p.Hq / p.Hkv);
+    const int64_t q_head = ((int64_t)t.b * p.Hq + t.hq) * p.Sq * D;
+    const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * D;
+    const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((char *)p.o + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
+
+    // Q^T is the B operand of S^T = K Q^T: lane holds Q[row][16kk + 8h .. +7]
+    // for each k-step.  The block's Q rows stay in LDS (same swizzle as K)
+    // rather than in registers; each wave copies its own 32 rows.
+    const int q_wave0 = t.m * BM + 32 * w;
+    const int my_q = q_wave0 + c;
+    // Tile copies straight into LDS: each instruction of a wave fills 1024
+    // contiguous LDS bytes (lane j at 16*j); wave w fills slots
+    // (w*IPW + i)*64 + lane of a tile, fetching the global chunk that the
+    // swizzled layout puts there.
+    uint32_t k_src[IPW], v_src[IPW];
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+        const int slot = (w * IPW + i) * 64 + lane;
+        const int row = slot / CHUNKS_PER_ROW;
+        const int phys = slot % CHUNKS_PER_ROW;
+        k_src[i] = row * ROW_BYTES + ((phys ^ k_swizzle<D>(row)) * 16);
+        const int seg = (phys >> 1) ^ v_swizzle<D>(row);
+        v_src[i] = row * ROW_BYTES + (seg * 2 + (phys & 1)) * 16;
+    }
+    const char *const k_head = (const char *)p.k + kv_head * 2;
+    const char *const v_head = (const char *)p.v + kv_head * 2;
+    const uint32_t kv_bytes = p.Skv * ROW_BYTES;
+    const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+    // Tile n of K or V into LDS at byte offset dst.  Tiles at or past Skv get a
+    // zero-size descriptor, so their copies write zeros.
+    auto copy_tile = [&](const char *head, const uint32_t *src, const int n, const uint32_t dst) __attribute__((always_inline)) {
+        const uint32_t off = (uint32_t)n * TILE_BYTES;
+        const uint32_t left = off < kv_bytes ? kv_bytes - off : 0u;
+        const i32x4 d = buffer_words(head + (off < kv_bytes ? off : 0u), left);
+#pragma unroll
+        for (int i = 0; i < IPW; ++i)
+            lds_copy16(d, src[i], lds_base + dst + (w * IPW + i) * 1024);
+    };
+    // Stage j = {K(j+1), V(j)} into buffer j % kStages.
+    auto copy_stage = [&](const int j) __attribute__((always_inline)) {
+        const uint32_t base = (uint32_t)(j % kStages) * STAGE_BYTES;
+        copy_tile(k_head, k_src, j + 1, base);
+        copy_tile(v_head, v_src, j, base + TILE_BYTES);
+    };
+
+    const int kv_end = CAUSAL ? min((t.m + 1) * BM, p.Skv) : p.Skv;
+    const int n_tiles = (kv_end + BN - 1) / BN;
+
+    // Per-lane LDS read offsets.
+    uint32_t k_off[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk)
+        k_off[kk] = c * ROW_BYTES + (((2 * kk + h) ^ k_swizzle<D>(c)) * 16);
+    const int li = lane & 15;
+    const int gsel = (lane >> 4) & 1;
+    uint32_t v_off[DBLK];
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+        v_off[db] = (4 * h + (li >> 2)) * ROW_BYTES + 8 * (li & 3) +
+                    (((2 * db + gsel) ^ v_swizzle<D>(4 * h + (li >> 2))) * 32);
+
+    // This wave's Q rows in LDS; row c (the lane's query) uses the same swizzle
+    // as K row c, so the Q operand offsets equal the K operand offsets.
+    lds_char *const q_wave = q_lds + w * 32 * ROW_BYTES;
+    bf16x8 qreg[kQInLds ? 1 : KSTEPS];
+    if constexpr (!kQInLds) {
+        const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)((const char *)p.q + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk)
+            qreg[kk] = __builtin_bit_cast(
+                bf16x8, load16(rq, (uint32_t)(my_q * D + 16 * kk + 8 * h) * 2u));
+    }
+    auto q_operand = [&](const int kk) __attribute__((always_inline)) -> bf16x8 {
+        if constexpr (kQInLds) return *(const lds_bf16x8 *)(q_wave + k_off[kk]);
+        else return qreg[kk];
+    };
+
+    f32x16 oacc[DBLK];
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+        for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
+    // Online-softmax state (see attn_fwd.hip): lazy reference maximum m_ref,
+    // raised only when a score exceeds it by more than 2^kLazy (exp2 domain).
+    float m_ref = -__builtin_inff();
+    float mb = -__builtin_inff();
+    // Row sums of P, accumulated on the matrix core: an all-ones A operand
+    // times P^T puts the sum over a 16-key chunk into every accumulator entry
+    // of the lane that owns the query row (no cross-lane reduction needed).
+    f32x16 lacc = {};
+    bf16x8 ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+    const float sl2 = p.scale_log2;
+
+    f32x16 s_cur[2];    // scores of the tile the next E step works on
+    bf16x8 pbuf[4];     // P of the tile the next G step multiplies, 4 chunks of 16 keys
+
+    // E(j): softmax of s_cur (tile j) into pbuf.
+    auto softmax_step = [&](const int j) __attribute__((always_inline)) {
+        const int key0 = j * BN;
+        const bool need_mask = (key0 + BN > p.Skv) || (CAUSAL && key0 + BN - 1 > q_wave0);
+        if (need_mask) {
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = key0 + 32 * kb2 + 8 * (r >> 2) + 4 * h + (r & 3);
+                    const bool dead = key >= p.Skv || (CAUSAL && key > my_q);
+                    s_cur[kb2][r] = dead ? -__builtin_inff() : s_cur[kb2][r];
+                }
+        }
+        float mx = s_cur[0][0];
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kb2][r]);
+        if (__any((mx - m_ref) * sl2 > kLazy)) {
+            const float m_new = fmaxf(m_ref, fmaxf(mx, xor32(mx)));
+            const float alpha = exp2_hw((m_ref - m_new) * sl2);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) lacc[r] *= alpha;
+#pragma unroll
+            for (int db = 0; db < DBLK; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+            m_ref = m_new;
+            mb = m_ref * sl2;
+        }
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) {
+            f32x8 p8;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                p8[e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
+            pbuf[kc] = __builtin_convertvector(p8, bf16x8);
+        }
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) anchor(pbuf[kc]);
+    };
+
+    // G(j): S(j+1) = K(j+1) Q^T into s_cur (free once P(j) is formed) and
+    // O^T += V(j)^T P(j)^T, stage j in LDS buffer (j % 2).  The 32 MFMAs
+    // alternate between the two products (even i: scores, odd i: output) and
+    // their A operands are read from LDS kPrefetch MFMAs ahead, so the matrix
+    // core does not wait for LDS latency.
+    auto gemm_step = [&](const int j, auto buf_c) __attribute__((always_inline)) {
+        constexpr int BUF = decltype(buf_c)::value;   // j % kStages
+        (void)j;
+        lds_char *const kb = lds + BUF * STAGE_BYTES;
+        lds_char *const vb = kb + TILE_BYTES;
+        f32x16 (&s_next)[2] = s_cur;
+        // A operand of MFMA i: a K row chunk (scores) or a V column chunk.
+        auto a_operand = [&](const int i) __attribute__((always_inline)) -> bf16x8 {
+            if ((i & 1) == 0) {
+                const int si = i >> 1, kk = si >> 1, kb2 = si & 1;
+                return *(const lds_bf16x8 *)(kb + k_off[kk] + kb2 * 32 * ROW_BYTES);
+            }
+            const int vi = i >> 1, kc = vi >> 2, db = vi & 3;
+            const int chunk = 16 * kc * ROW_BYTES;
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (lds_bf16x4 *)(vb + v_off[db] + chunk));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (lds_bf16x4 *)(vb + v_off[db] + chunk + 8 * ROW_BYTES));
+            return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        };
+        bf16x8 ring[kPrefetch];
+        bf16x8 qop[2];
+#pragma unroll
+        for (int i = 0; i < kPrefetch; ++i) ring[i] = a_operand(i);
+        qop[0] = q_operand(0);
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+            const bf16x8 a = ring[i % kPrefetch];
+            if (i + kPrefetch < 32) ring[i % kPrefetch] = a_operand(i + kPrefetch);
+            if ((i & 1) == 0) {
+                const int si = i >> 1, kk = si >> 1, kb2 = si & 1;
+                // the Q operand of the next k-step, read one score-MFMA pair ahead
+                if (kb2 == 0 && kk + 1 < KSTEPS) qop[(kk + 1) & 1] = q_operand(kk + 1);
+                const f32x16 zero = {};
+                s_next[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    a, qop[kk & 1], kk == 0 ? zero : s_next[kb2], 0, 0, 0);
+            } else {
+                const int vi = i >> 1, kc = vi >> 2, db = vi & 3;
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pbuf[kc], oacc[db], 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc)
+            lacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pbuf[kc], lacc, 0, 0, 0);
+        // Pin the order above: the prologue reads, then per MFMA i the reads
+        // for MFMA i+kPrefetch (and the next Q operand) followed by MFMA i,
+        // then the four row-sum MFMAs.
+        gemm_schedule_impl<kPrefetch>();
+        anchor(s_next[0]);
+        anchor(s_next[1]);
+#pragma unroll
+        for (int db = 0; db < DBLK; ++db) anchor(oacc[db]);
+        anchor(lacc);
+    };
+
+    // Prologue: this wave's Q rows, K(0) into the K slot of buffer 1, stage 0
+    // into buffer 0; S(0).
+    if constexpr (kQInLds) {
+        const char *const q_base = (const char *)p.q + q_head * 2;
+        const uint32_t q_bytes = p.Sq * ROW_BYTES;
+        const uint32_t off = (uint32_t)q_wave0 * ROW_BYTES;   // 32 rows = 8 KiB
+        const i32x4 d = buffer_words(q_base + (off < q_bytes ? off : 0u),
+                                     off < q_bytes ? q_bytes - off : 0u);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int slot = i * 64 + lane;                 // 16-byte slot within the 32 rows
+            const int row = slot / CHUNKS_PER_ROW;
+            const int phys = slot % CHUNKS_PER_ROW;
+            lds_copy16(d, row * ROW_BYTES + ((phys ^ k_swizzle<D>(row)) * 16),
+                       lds_base + 2 * STAGE_BYTES + w * 32 * ROW_BYTES + i * 1024);
+        }
+    }
+    // K(0) goes into the K slot of the last buffer, which stage kStages-1
+    // (issued after the scores of tile 0 are computed) later overwrites.
+    copy_tile(k_head, k_src, 0, (kStages - 1) * STAGE_BYTES);
+    for (int j = 0; j < kAhead && j < n_tiles; ++j) copy_stage(j);
+    barrier_lds_copies();
+    {
+        lds_char *const kb = lds + (kStages - 1) * STAGE_BYTES;
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+            for (int r = 0; r < 16; ++r) s_cur[kb2][r] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk) {
+            const bf16x8 qop = q_operand(kk);
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2) {
+                const bf16x8 a = *(const lds_bf16x8 *)(kb + k_off[kk] + kb2 * 32 * ROW_BYTES);
+                s_cur[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop, s_cur[kb2], 0, 0, 0);
+            }
+        }
+    }
+
+    // Every wave runs E(0) G(0) E(1) G(1) ... with a barrier after each step;
+    // group B starts one barrier late (and group A ends with one extra), so
+    // the groups stay one phase apart.  Stage k+kAhead is copied at global
+    // phase 2k+1 -- by A before G(k), by B before E(k) -- into the buffer of
+    // stage k+kAhead-kStages, which both groups finished reading by phase 2k.
+    // Stage k is read from phase 2k+1 on, so every wave's share of it must
+    // have landed by the barrier that starts that phase.
+    if (grp == 1) barrier_lds();
+    auto tile = [&](const int k, auto buf_c) __attribute__((always_inline)) {
+        if (grp == 1 && k + kAhead < n_tiles) copy_stage(k + kAhead);
+        softmax_step(k);
+        // A, before its G(k): stage k has landed; stages up to k+kAhead-1 may fly.
+        if (grp == 0) wait_copies(min(kAhead - 1, n_tiles - 1 - k));
+        barrier_lds();
+        if (grp == 0 && k + kAhead < n_tiles) copy_stage(k + kAhead);
+        gemm_step(k, buf_c);
+        // B, before A's G(k+1): stage k+1 has landed; up to k+kAhead may fly.
+        if (grp == 1) wait_copies(min(kAhead - 1, n_tiles - 2 - k));
+        barrier_lds();
+    };
+    // kStages tiles per trip, so that every LDS buffer offset is an immediate.
+    static_assert(kStages == 2, "the trip below is written for two stages");
+    for (int k = 0; k < n_tiles; k += 2) {
+        tile(k, Int<0>{});
+        if (k + 1 < n_tiles) tile(k + 1, Int<1>{});
+    }
+    if (grp == 0) barrier_lds();
+
+    // O = acc / l, rounded to bf16; lane holds d = 32db + 8j + 4h + 0..3 of its row.
+    const float inv = 1.0f / lacc[0];
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const f32x4 o4 = {oacc[db][4 * jj + 0] * inv, oacc[db][4 * jj + 1] * inv,
+                              oacc[db][4 * jj + 2] * inv, oacc[db][4 * jj + 3] * inv};
+            const bf16x4 ob = __builtin_convertvector(o4, bf16x4);
+            const uint32_t off = (uint32_t)(my_q * D + 32 * db + 8 * jj + 4 * h) * 2u;
+            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ob), ro, (int)off, 0, 0);
+        }
+    }
+}
+
+template <bool CAUSAL, int MAPPING>
+hipError_t launch_pp(const KernelArgs &a, int grid, hipStream_t stream) {
+    if (a.heavy_first)
+        hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, true>), dim3(grid),
+                           dim3(kPPThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, false>), dim3(grid),
+                           dim3(kPPThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <bool CAUSAL>
+hipError_t launch_pp_mapping(const KernelArgs &a, int mapping, int grid, hipStream_t stream) {
+    switch (mapping) {
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_pp<CAUSAL, 0>(a, grid, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_pp<CAUSAL, 1>(a, grid, stream);
+        default: return launch_pp<CAUSAL, 2>(a, grid, stream);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_fwd_d128(const KernelArgs &a, bool causal, int mapping, int grid,
+                                hipStream_t stream) {
+    return causal ? launch_pp_mapping<true>(a, mapping, grid, stream)
+                  : launch_pp_mapping<false>(a, mapping, grid, stream);
+}
+
+}  // namespace attn

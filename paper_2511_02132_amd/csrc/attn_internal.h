@@ -7,9 +7,15 @@
 
 namespace attn {
 
-// Query rows per workgroup and keys per K/V tile (Section 4.3 uses 128 x 64).
-constexpr int kBlockM = 128;
+// Query rows per workgroup and keys per K/V tile.  Section 4.3 uses 128 x 64;
+// the head-dimension-128 kernel runs two wave groups over 256 rows per
+// workgroup so that each K/V tile copied into LDS serves twice as many rows.
+constexpr int kBlockM = 128;      // d = 64 (4 waves)
+constexpr int kBlockM128 = 256;   // d = 128 (8 waves, two groups)
 constexpr int kBlockN = 64;
+constexpr int kMaxBlockM = 256;
+
+__host__ __device__ constexpr int block_m_for(int d) { return d == 128 ? kBlockM128 : kBlockM; }
 
 // Kernel arguments; tensors are bf16, BHSD contiguous.
 struct KernelArgs {
@@ -19,7 +25,7 @@ struct KernelArgs {
     void *o;
     int32_t *probe;   // NULL, or 4 int32 per workgroup: b, hq, m, xcc
     int B, Hq, Hkv, Sq, Skv;
-    int NB;           // ceil(Sq / kBlockM)
+    int NB;           // ceil(Sq / block_m_for(d))
     int NX;           // XCD count used by the mapping
     int heavy_first;  // ATTN_ORDER_HEAVY_FIRST was set
     float scale_log2; // scale * log2(e): softmax evaluated with exp2
@@ -72,5 +78,8 @@ __host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, 
 // 0/1/2 (one kernel instantiation per combination).
 hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int mapping, int grid,
                            hipStream_t stream);
+// The head-dimension-128 kernel (attn_fwd_pp.hip).
+hipError_t launch_attn_fwd_d128(const KernelArgs &args, bool causal, int mapping, int grid,
+                                hipStream_t stream);
 
 }  // namespace attn

@@ -94,7 +94,7 @@ def summarise(dirs, workload: str):
         rows = read_csv(d)
         for did, kname, grid, cname, val in rows:
             v = variant_of(kname)
-            if v is not None and grid == 256:
+            if v is not None and grid <= 512:   # the one-workgroup launch
                 one_wg_dispatches.append((d, did))
                 continue
             if v is not None:

@@ -73,12 +73,13 @@ def test_probe_validation():
 
 
 def test_sizes():
-    assert pa.block_m(64) == pa.block_m(128) == 128
+    assert pa.block_m(64) == 128 and pa.block_m(128) == 256
     assert pa.block_n(64) == pa.block_n(128) == 64
     assert pa.lib().attn_block_m(96) == -3
-    assert pa.grid_size(1, 32, 8192, 128) == 2048
-    assert pa.grid_size(8, 64, 4096, 128) == 16384
+    assert pa.grid_size(1, 32, 8192, 128) == 1024
+    assert pa.grid_size(8, 64, 4096, 128) == 8192
     assert pa.grid_size(2, 3, 129, 64) == 12
+    assert pa.grid_size(2, 3, 257, 128) == 12
     assert pa.lib().attn_grid_size(1, 1, 0, 128) == -2
 
 
