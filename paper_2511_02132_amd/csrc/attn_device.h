@@ -46,11 +46,15 @@ __device__ __forceinline__ i32x4 buffer_words(const void *base, uint32_t bytes) 
 // these copies itself (vmcnt) before the barrier that publishes a tile.
 // M0 is a register the compiler reserves; these kernels give it no other use
 // (a CPU test compiles them and checks that every instruction reading M0 is one
-// of these copies, each right after its own M0 write).
+// of these copies, each right after its own M0 write).  The compiler's hazard
+// pass does not look inside the assembly, so the wait states are explicit: one
+// between the M0 write and the load that reads it, and at least five between
+// a vector-ALU write of a descriptor word (v_readfirstlane) and the load that
+// reads it -- the s_mov and the s_nop 4 supply six.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void lds_copy16(i32x4 rsrc, uint32_t voffset, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 4\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                  :
                  : "v"(voffset), "s"(rsrc), "s"(lds_addr)
                  : "memory", "m0");

@@ -12,10 +12,9 @@
 // 4-7 (rows 128..255); both stream the same K/V tiles of 64 keys.
 //
 // Per tile j a group does two steps:
-//   E(j): softmax of S(j): mask, lazy running max, P = exp2(...), P -> bf16
-//         (vector ALU);
-//   G(j): S(j+1) = K(j+1) Q^T, O^T += V(j)^T P(j)^T and the row sums of P(j)
-//         (36 MFMAs).
+//   E(j): softmax of S(j): mask, lazy running max, P = exp2(...), the row
+//         sums of P, P -> bf16 (vector ALU);
+//   G(j): S(j+1) = K(j+1) Q^T and O^T += V(j)^T P(j)^T (32 MFMAs).
 // The groups run these one phase apart, phases separated by workgroup
 // barriers:
 //   phase 2k:   A: E(k)   B: G(k-1)
@@ -83,13 +82,13 @@ __host__ __device__ constexpr int a_reads(int i) { return (i & 1) ? 2 : 1; }
 // then per MFMA i the reads for MFMA i+PF (and, before each even k-step, the
 // next Q operand) followed by MFMA i.
 __host__ __device__ constexpr int prologue_reads(int pf) {
-    int n = 1;   // Q operand of k-step 0
+    int n = kQInLds ? 1 : 0;   // Q operand of k-step 0
     for (int i = 0; i < pf; ++i) n += a_reads(i);
     return n;
 }
 __host__ __device__ constexpr int step_reads(int pf, int i) {
     return (i + pf < 32 ? a_reads(i + pf) : 0) +
-           (((i & 1) == 0 && ((i >> 1) & 1) == 0 && (i >> 2) + 1 < 8) ? 1 : 0);
+           ((kQInLds && (i & 1) == 0 && ((i >> 1) & 1) == 0 && (i >> 2) + 1 < 8) ? 1 : 0);
 }
 template <int PF, int I>
 __device__ __forceinline__ void gemm_schedule_step() {
@@ -104,7 +103,6 @@ template <int PF>
 __device__ __forceinline__ void gemm_schedule_impl() {
     __builtin_amdgcn_sched_group_barrier(kSchedDsRead, prologue_reads(PF), 0);
     gemm_schedule_step<PF, 0>();
-    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4, 0);
 }
 
 // Wait until at most 4*n copy instructions (the n newest stages) are in flight.
@@ -183,12 +181,16 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     const char *const v_head = (const char *)p.v + kv_head * 2;
     const uint32_t kv_bytes = p.Skv * ROW_BYTES;
     const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
-    // Tile n of K or V into LDS at byte offset dst.  Tiles at or past Skv get a
-    // zero-size descriptor, so their copies write zeros.
+    const int kv_end = CAUSAL ? min((t.m + 1) * BM, p.Skv) : p.Skv;
+    const int n_tiles = (kv_end + BN - 1) / BN;
+    // Tile n of K or V into LDS at byte offset dst.  The descriptor ends at the
+    // block's last tile (or at Skv), so copies of tiles beyond write zeros and
+    // fetch nothing (the last product step's K(n_tiles) among them).
+    const uint32_t kv_lim = min(kv_bytes, (uint32_t)n_tiles * TILE_BYTES);
     auto copy_tile = [&](const char *head, const uint32_t *src, const int n, const uint32_t dst) __attribute__((always_inline)) {
         const uint32_t off = (uint32_t)n * TILE_BYTES;
-        const uint32_t left = off < kv_bytes ? kv_bytes - off : 0u;
-        const i32x4 d = buffer_words(head + (off < kv_bytes ? off : 0u), left);
+        const uint32_t left = off < kv_lim ? kv_lim - off : 0u;
+        const i32x4 d = buffer_words(head + (off < kv_lim ? off : 0u), left);
 #pragma unroll
         for (int i = 0; i < IPW; ++i)
             lds_copy16(d, src[i], lds_base + dst + (w * IPW + i) * 1024);
@@ -199,9 +201,6 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
         copy_tile(k_head, k_src, j + 1, base);
         copy_tile(v_head, v_src, j, base + TILE_BYTES);
     };
-
-    const int kv_end = CAUSAL ? min((t.m + 1) * BM, p.Skv) : p.Skv;
-    const int n_tiles = (kv_end + BN - 1) / BN;
 
     // Per-lane LDS read offsets.
     uint32_t k_off[KSTEPS];
@@ -241,13 +240,9 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     // raised only when a score exceeds it by more than 2^kLazy (exp2 domain).
     float m_ref = -__builtin_inff();
     float mb = -__builtin_inff();
-    // Row sums of P, accumulated on the matrix core: an all-ones A operand
-    // times P^T puts the sum over a 16-key chunk into every accumulator entry
-    // of the lane that owns the query row (no cross-lane reduction needed).
-    f32x16 lacc = {};
-    bf16x8 ones;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+    // Row sum of P over this lane's keys (the lane l^32 holds the row's other
+    // keys; the two halves are added once, at the end).
+    float lsum = 0.0f;
     const float sl2 = p.scale_log2;
 
     f32x16 s_cur[2];    // scores of the tile the next E step works on
@@ -275,8 +270,7 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
         if (__any((mx - m_ref) * sl2 > kLazy)) {
             const float m_new = fmaxf(m_ref, fmaxf(mx, xor32(mx)));
             const float alpha = exp2_hw((m_ref - m_new) * sl2);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) lacc[r] *= alpha;
+            lsum *= alpha;
 #pragma unroll
             for (int db = 0; db < DBLK; ++db)
 #pragma unroll
@@ -290,6 +284,8 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 p8[e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
+#pragma unroll
+            for (int e = 0; e < 8; ++e) lsum += p8[e];
             pbuf[kc] = __builtin_convertvector(p8, bf16x8);
         }
 #pragma unroll
@@ -321,6 +317,12 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
                 (lds_bf16x4 *)(vb + v_off[db] + chunk + 8 * ROW_BYTES));
             return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         };
+        // The wave feeding the matrix core gets issue priority over the
+        // softmax wave sharing its SIMD (by default the older wave, group A,
+        // would win every conflict and slow group B's MFMAs).
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+        __builtin_amdgcn_sched_barrier(0);
         bf16x8 ring[kPrefetch];
         bf16x8 qop[2];
 #pragma unroll
@@ -342,18 +344,17 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
                 oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pbuf[kc], oacc[db], 0, 0, 0);
             }
         }
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc)
-            lacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pbuf[kc], lacc, 0, 0, 0);
         // Pin the order above: the prologue reads, then per MFMA i the reads
-        // for MFMA i+kPrefetch (and the next Q operand) followed by MFMA i,
-        // then the four row-sum MFMAs.
+        // for MFMA i+kPrefetch (and the next Q operand) followed by MFMA i.
         gemm_schedule_impl<kPrefetch>();
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
         anchor(s_next[0]);
         anchor(s_next[1]);
 #pragma unroll
         for (int db = 0; db < DBLK; ++db) anchor(oacc[db]);
-        anchor(lacc);
+
     };
 
     // Prologue: this wave's Q rows, K(0) into the K slot of buffer 1, stage 0
@@ -423,7 +424,7 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     if (grp == 0) barrier_lds();
 
     // O = acc / l, rounded to bf16; lane holds d = 32db + 8j + 4h + 0..3 of its row.
-    const float inv = 1.0f / lacc[0];
+    const float inv = 1.0f / (lsum + xor32(lsum));
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
 #pragma unroll

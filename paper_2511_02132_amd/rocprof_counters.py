@@ -5,7 +5,8 @@ Each pass directory holds one rocprofv3 run (``-d DIR -o run -f csv json``) of
     rocprofv3 --pmc <counters> -d DIR -o run -f csv json -- python3 bench.py --profile --workload W
 
 Every (mapping, block order) of the attention kernel is its own kernel symbol
-(``attn_fwd_kernel<d, causal, mapping, heavy_first>``), so one run per pass
+(``attn_fwd_kernel<d, causal, mapping, heavy_first>`` or, for d = 128,
+``attn_fwd_pp_kernel<causal, mapping, heavy_first>``), so one run per pass
 covers all variants.  The run also holds a one-workgroup launch (it can only
 run on XCD 0) and a 256 MiB device copy, used to attribute counter instances
 to XCDs and to scale FETCH_SIZE / WRITE_SIZE to bytes.
@@ -28,15 +29,17 @@ import sys
 from collections import defaultdict
 
 MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first"]
-KERNEL_RE = re.compile(r"attn_fwd_kernel<(\d+), (true|false), (\d), (true|false)>")
+# attn_fwd_kernel<d, causal, mapping, heavy_first> (4-wave kernel) and
+# attn_fwd_pp_kernel<causal, mapping, heavy_first> (d = 128 two-group kernel)
+KERNEL_RE = re.compile(r"attn_fwd_(?:kernel<\d+, |pp_kernel<)(true|false), (\d), (true|false)>")
 
 
 def variant_of(kernel_name: str):
     m = KERNEL_RE.search(kernel_name)
     if not m:
         return None
-    name = MAPPING_NAMES[int(m.group(3))]
-    return name + ("+heavy_first" if m.group(4) == "true" else "")
+    name = MAPPING_NAMES[int(m.group(2))]
+    return name + ("+heavy_first" if m.group(3) == "true" else "")
 
 
 def read_csv(d: str):
