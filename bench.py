@@ -15,7 +15,7 @@ line:
               WRITE_SIZE (scaled by a copy kernel of known size), read from
               the committed counter summary when it was taken on this kernel
               source, else null
-  per_mapping TFLOP/s of all three mappings (and, for causal workloads, each
+  per_mapping TFLOP/s of all four mappings (and, for causal workloads, each
               with the heavy-first block order), interleaved, cold (L2 and MALL
               flushed before every launch) and warm, median over reps, plus the
               L2 hit rate from the counter summary
@@ -41,7 +41,8 @@ DEFAULT_WORKLOAD = "mha_b1_h32_s8192_d128_causal"
 METRIC = "attention fwd TFLOP/s (% of bf16 MFMA peak) + L2 hit rate, per mapping"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first"]
+MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
+                 "swizzled_block_first"]
 HEAVY_FIRST = 0x10
 
 

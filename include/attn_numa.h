@@ -12,6 +12,11 @@
  *   ATTN_MAP_NAIVE_HEAD_FIRST    -- head-major order (Section 3.2)
  *   ATTN_MAP_SWIZZLED_HEAD_FIRST -- head-major order cut into one contiguous
  *                                   piece per XCD (Section 3.3, the method)
+ *   ATTN_MAP_SWIZZLED_BLOCK_FIRST -- block-major order with each row block's
+ *                                   heads renumbered so that one XCD gets a
+ *                                   contiguous range of them, keeping a GQA
+ *                                   group on one XCD (Section 3.2; the paper
+ *                                   gives no formula, see map_tiles below)
  *
  * The hardware dispatches WG `wid` to XCD `wid mod NX` (Section 2.2); each
  * mapping is a permutation wid -> (b, hq, m) computed in the kernel prologue.
@@ -34,6 +39,7 @@ enum {
     ATTN_MAP_NAIVE_BLOCK_FIRST = 0,
     ATTN_MAP_NAIVE_HEAD_FIRST = 1,
     ATTN_MAP_SWIZZLED_HEAD_FIRST = 2,
+    ATTN_MAP_SWIZZLED_BLOCK_FIRST = 3,
     /* Optional flag OR-ed into any mapping: dispatch each head's row blocks
      * from the last to the first (m -> NB-1-m).  The XCD that runs each
      * (batch, head) is unchanged; under a causal mask, where block m costs m+1
@@ -73,7 +79,8 @@ enum {
  * scale : finite and > 0 (the paper uses 1/sqrt(d)); softmax is taken in fp32
  *     with bf16 inputs, fp32 accumulation and bf16 rounding (RNE) of P and O.
  * mapping : one of ATTN_MAP_NAIVE_BLOCK_FIRST, ATTN_MAP_NAIVE_HEAD_FIRST,
- *     ATTN_MAP_SWIZZLED_HEAD_FIRST, optionally | ATTN_ORDER_HEAVY_FIRST.
+ *     ATTN_MAP_SWIZZLED_HEAD_FIRST, ATTN_MAP_SWIZZLED_BLOCK_FIRST, optionally
+ *     | ATTN_ORDER_HEAVY_FIRST.
  *
  * Ownership: all buffers belong to the caller; nothing is retained after the
  * call returns and nothing is allocated.  The kernel is enqueued on the stream

@@ -33,6 +33,15 @@ The three mappings (integer ``mapping`` argument of the C ABI):
      not, where the first r XCDs take one WG more.  Batch is outermost
      throughout (the readings of the garbled per-batch line of the listing and
      of Hq < NX are recorded with the design notes).
+  3  swizzled block-first (Section 3.2): block-first order, with the query
+     heads of every (batch, row block) row renumbered so that the WGs one XCD
+     receives from that row carry a contiguous range of heads -- so the heads
+     of a GQA group land on one XCD when the group count equals NX.  The
+     paper gives no formula; this is the chiplet swizzle applied within each
+     row of Hq WGs: position j of the row (its WG goes to XCD
+     (row start + j) mod NX) takes head (j mod NX)*qh + min(j mod NX, rh) +
+     j div NX, with qh, rh = divmod(Hq, NX).  When NX divides Hq, XCD x gets
+     heads x*Hq/NX .. (x+1)*Hq/NX - 1 of every row block.
 
 Order option (not one of the paper's mappings): ``heavy_first`` replaces the
 row block m by NB-1-m after any mapping, so every (b, hq) keeps its XCD but
@@ -47,7 +56,8 @@ import numpy as np
 NAIVE_BLOCK_FIRST = 0
 NAIVE_HEAD_FIRST = 1
 SWIZZLED_HEAD_FIRST = 2
-MAPPINGS = (NAIVE_BLOCK_FIRST, NAIVE_HEAD_FIRST, SWIZZLED_HEAD_FIRST)
+SWIZZLED_BLOCK_FIRST = 3
+MAPPINGS = (NAIVE_BLOCK_FIRST, NAIVE_HEAD_FIRST, SWIZZLED_HEAD_FIRST, SWIZZLED_BLOCK_FIRST)
 
 
 def num_row_blocks(Sq: int, BM: int) -> int:
@@ -94,6 +104,9 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
         b, hq, m = unravel(wid, (B, Hq, NB))
     elif mapping == SWIZZLED_HEAD_FIRST:
         b, hq, m = unravel(swizzled_rank(wid, N, NX), (B, Hq, NB))
+    elif mapping == SWIZZLED_BLOCK_FIRST:
+        b, m, j = unravel(wid, (B, NB, Hq))
+        hq = swizzled_rank(j, Hq, NX)
     else:
         raise ValueError("unknown mapping %r" % (mapping,))
     if heavy_first:

@@ -22,10 +22,11 @@ import numpy as np
 NAIVE_BLOCK_FIRST = 0
 NAIVE_HEAD_FIRST = 1
 SWIZZLED_HEAD_FIRST = 2
+SWIZZLED_BLOCK_FIRST = 3
 # Flag OR-ed into a mapping: dispatch each head's row blocks last-to-first.
 HEAVY_FIRST = 0x10
 MAPPINGS = {"naive_block_first": NAIVE_BLOCK_FIRST, "naive_head_first": NAIVE_HEAD_FIRST,
-            "swizzled_head_first": SWIZZLED_HEAD_FIRST}
+            "swizzled_head_first": SWIZZLED_HEAD_FIRST, "swizzled_block_first": SWIZZLED_BLOCK_FIRST}
 
 ATTN_OK = 0
 ATTN_ERR = {-1: "ATTN_ERR_NULL", -2: "ATTN_ERR_SHAPE", -3: "ATTN_ERR_UNSUPPORTED",

@@ -48,7 +48,7 @@ int check_shape(int B, int Hq, int Hkv, int Sq, int Skv, int d) {
 bool valid_mapping(int mapping) {
     const int base = mapping & 0xf;
     const int flags = mapping & ~0xf;
-    return base >= ATTN_MAP_NAIVE_BLOCK_FIRST && base <= ATTN_MAP_SWIZZLED_HEAD_FIRST &&
+    return base >= ATTN_MAP_NAIVE_BLOCK_FIRST && base <= ATTN_MAP_SWIZZLED_BLOCK_FIRST &&
            (flags & ~ATTN_ORDER_HEAVY_FIRST) == 0;
 }
 
@@ -183,7 +183,7 @@ const char *attn_strerror(int code) {
         case ATTN_ERR_NULL: return "null pointer argument";
         case ATTN_ERR_SHAPE: return "invalid shape (non-positive dimension, Hq % Hkv != 0, or size limit)";
         case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (supported: 64, 128)";
-        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, optionally | ATTN_ORDER_HEAVY_FIRST)";
+        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST)";
         case ATTN_ERR_SCALE: return "scale must be finite and > 0";
         case ATTN_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
         case ATTN_ERR_HIP: return "HIP runtime error";

@@ -12,7 +12,7 @@
 //
 // Placement (Sections 2.2, 3.2, 3.3): the hardware dispatches WG id `wid` to XCD
 // `wid mod NX`; the prologue turns `wid` into the tile (b, hq, m) by one of
-// three permutations, so the mapping alone decides which XCD's private L2 a
+// four permutations, so the mapping alone decides which XCD's private L2 a
 // head's K/V stream goes through:
 //   0 naive block-first:   (b, m, hq) = digits of wid, heads fastest
 //   1 naive head-first:    (b, hq, m) = digits of wid, blocks fastest
@@ -21,6 +21,12 @@
 //     k = wid div NX and (q, r) = divmod(N, NX), L = x*q + min(x, r) + k.
 //     XCD x then runs one contiguous piece of the head-major order, i.e. whole
 //     heads (whole K/V groups under GQA), one after another.
+//   3 swizzled block-first: block-major like 0, with the heads of each row
+//     block renumbered (the same XCD-major rank, within the row of Hq WGs) so
+//     that one XCD gets a contiguous range of heads -- a GQA group when the
+//     group count equals NX.
+// (map_wid in attn_internal.h.)  This kernel serves head dimension 64; head
+// dimension 128 runs the two-group kernel of attn_fwd_pp.hip.
 //
 // Work split inside a WG (256 threads = 4 waves of 64 lanes, one per SIMD):
 // wave w owns query rows 32w..32w+31 of the block.  Both contractions use
@@ -317,7 +323,8 @@ hipError_t launch_mapping(const KernelArgs &a, int mapping, int grid, hipStream_
     switch (mapping) {
         case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_one<D, CAUSAL, 0>(a, grid, stream);
         case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_one<D, CAUSAL, 1>(a, grid, stream);
-        default: return launch_one<D, CAUSAL, 2>(a, grid, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_one<D, CAUSAL, 2>(a, grid, stream);
+        default: return launch_one<D, CAUSAL, 3>(a, grid, stream);
     }
 }
 

@@ -454,7 +454,8 @@ hipError_t launch_pp_mapping(const KernelArgs &a, int mapping, int grid, hipStre
     switch (mapping) {
         case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_pp<CAUSAL, 0>(a, grid, stream);
         case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_pp<CAUSAL, 1>(a, grid, stream);
-        default: return launch_pp<CAUSAL, 2>(a, grid, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_pp<CAUSAL, 2>(a, grid, stream);
+        default: return launch_pp<CAUSAL, 3>(a, grid, stream);
     }
 }
 

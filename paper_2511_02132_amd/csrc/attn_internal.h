@@ -35,7 +35,7 @@ struct Tile {
     int b, hq, m;
 };
 
-// Workgroup id -> tile (b, hq, m) for base mapping 0/1/2 (ATTN_MAP_*);
+// Workgroup id -> tile (b, hq, m) for base mapping 0..3 (ATTN_MAP_*);
 // integer only.  In the kernel the arguments are uniform, so this runs on the
 // scalar unit.
 //   0 naive block-first:   digits of wid over (B, NB, Hq), heads fastest
@@ -43,17 +43,28 @@ struct Tile {
 //   2 swizzled head-first: digits over (B, Hq, NB) of the rank of wid in the
 //     XCD-major listing of the grid (XCD x = wid mod NX receives its k-th WG
 //     as wid = x + k*NX; the first N mod NX XCDs hold one WG more).
+//   3 swizzled block-first: as 0, but within each (b, m) row of Hq WGs the
+//     position j takes head (j mod NX)*qh + min(j mod NX, rh) + j div NX,
+//     (qh, rh) = divmod(Hq, NX): the WGs of a row that one XCD receives carry
+//     contiguous heads, so a GQA group stays on one XCD when Hkv == NX.
 // heavy_first (ATTN_ORDER_HEAVY_FIRST) then replaces m by NB-1-m: the XCD of
 // every (b, hq) is unchanged, but each head's row blocks are dispatched from
 // the last (under a causal mask the most expensive) to the first.
 __host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, int B, int Hq,
                                         int NB, int NX) {
     Tile t;
-    if (mapping == 0) {
-        t.hq = wid % Hq;
+    if (mapping == 0 || mapping == 3) {
+        int j = wid % Hq;
         const int rest = wid / Hq;
         t.m = rest % NB;
         t.b = rest / NB;
+        if (mapping == 3) {
+            const int x = j % NX;
+            const int qh = Hq / NX;
+            const int rh = Hq % NX;
+            j = x * qh + (x < rh ? x : rh) + j / NX;
+        }
+        t.hq = j;
         if (heavy_first) t.m = NB - 1 - t.m;
         return t;
     }
@@ -75,7 +86,7 @@ __host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, 
 }
 
 // Enqueue the forward kernel for head dimension d (64 or 128) and base mapping
-// 0/1/2 (one kernel instantiation per combination).
+// 0..3 (one kernel instantiation per combination).
 hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int mapping, int grid,
                            hipStream_t stream);
 // The head-dimension-128 kernel (attn_fwd_pp.hip).

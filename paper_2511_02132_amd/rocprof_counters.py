@@ -28,7 +28,8 @@ import re
 import sys
 from collections import defaultdict
 
-MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first"]
+MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
+                 "swizzled_block_first"]
 # attn_fwd_kernel<d, causal, mapping, heavy_first> (4-wave kernel) and
 # attn_fwd_pp_kernel<causal, mapping, heavy_first> (d = 128 two-group kernel)
 KERNEL_RE = re.compile(r"attn_fwd_(?:kernel<\d+, |pp_kernel<)(true|false), (\d), (true|false)>")

@@ -1,0 +1,249 @@
+"""Mapping sweeps of the paper's sensitivity studies, on one MI355X.
+
+* MHA (Section 4.3, Table "mha_sweep"): context 8K/32K/128K x batch 1/2/4/8 x
+  heads (Hq = Hkv) 8/16/32/64/128, head dimension 128.
+* GQA (Section 4.4): eight KV heads, Hq = 32/64/128, same contexts and batches.
+
+Every configuration runs every mapping (four of Sections 3.2-3.3, each with
+and without the heavy-first block order when causal), interleaved within a
+repetition, each launch after an L2 + MALL flush, timed with HIP events on the
+launch stream; the median is reported, and each mapping relative to swizzled
+head-first (the paper's normalisation).  Inputs are N(0,1) bf16 drawn on the
+device with a seeded generator: the sweep only times the kernel, and the
+largest MHA shape (B8, H128, 128K: 137 GB of Q, K, V, O) is drawn on the GPU
+rather than on the host.
+
+    python -m paper_2511_02132_amd.sweep --family mha [--reps 2] [--json OUT.jsonl]
+    python -m paper_2511_02132_amd.sweep --family gqa --profile --manifest M.json
+        (one launch per variant, for rocprofv3 --pmc; writes the launch order)
+    Timed runs make one untimed launch per configuration first.
+    python -m paper_2511_02132_amd.sweep --summarise --timing OUT.jsonl
+        [--counters DIR --manifest M.json] --out profiles/FILE.md
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import json
+import os
+import statistics
+import sys
+
+MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
+                 "swizzled_block_first"]
+HEAVY_FIRST = 0x10
+CONTEXTS = (8192, 32768, 131072)
+BATCHES = (1, 2, 4, 8)
+MHA_HEADS = (8, 16, 32, 64, 128)
+GQA_QHEADS = (32, 64, 128)
+GQA_KV_HEADS = 8
+D = 128
+
+
+def variants(causal: bool):
+    out = [(n, i) for i, n in enumerate(MAPPING_NAMES)]
+    if causal:
+        out += [(n + "+heavy_first", i | HEAVY_FIRST) for i, n in enumerate(MAPPING_NAMES)]
+    return out
+
+
+def configs(family: str, contexts, batches, heads):
+    for S in contexts:
+        for B in batches:
+            for H in heads:
+                if family == "mha":
+                    yield {"B": B, "Hq": H, "Hkv": H, "S": S}
+                else:
+                    yield {"B": B, "Hq": H, "Hkv": GQA_KV_HEADS, "S": S}
+
+
+def flops(c, causal):
+    f = 4.0 * c["B"] * c["Hq"] * c["S"] * c["S"] * D
+    return f / 2 if causal else f
+
+
+def parse(argv=None):
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--family", choices=("mha", "gqa"), default="mha")
+    p.add_argument("--contexts", type=int, nargs="+", default=list(CONTEXTS))
+    p.add_argument("--batches", type=int, nargs="+", default=list(BATCHES))
+    p.add_argument("--heads", type=int, nargs="+", default=None,
+                   help="query heads (default: the paper's list for the family)")
+    p.add_argument("--non-causal", action="store_true")
+    p.add_argument("--reps", type=int, default=2)
+    p.add_argument("--json", default=None, help="append one JSON line per configuration")
+    p.add_argument("--profile", action="store_true")
+    p.add_argument("--manifest", default=None)
+    p.add_argument("--summarise", action="store_true")
+    p.add_argument("--timing", nargs="*", default=[])
+    p.add_argument("--counters", default=None)
+    p.add_argument("--out", default=None)
+    p.add_argument("--cmd", default="")
+    a = p.parse_args(argv)
+    if a.heads is None:
+        a.heads = list(MHA_HEADS if a.family == "mha" else GQA_QHEADS)
+    return a
+
+
+def run(a):
+    import torch
+
+    import paper_2511_02132_amd as pa
+
+    causal = not a.non_causal
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device=dev)
+    gen = torch.Generator(device=dev)
+    vs = variants(causal)
+    manifest = []
+    out = open(a.json, "a") if a.json else None
+    for ci, c in enumerate(configs(a.family, a.contexts, a.batches, a.heads)):
+        gen.manual_seed(7919 * ci + 1)
+        shape_q = (c["B"], c["Hq"], c["S"], D)
+        shape_kv = (c["B"], c["Hkv"], c["S"], D)
+        q = torch.randn(shape_q, generator=gen, device=dev, dtype=torch.bfloat16)
+        k = torch.randn(shape_kv, generator=gen, device=dev, dtype=torch.bfloat16)
+        v = torch.randn(shape_kv, generator=gen, device=dev, dtype=torch.bfloat16)
+        o = torch.empty_like(q)
+        scale = 1.0 / D ** 0.5
+        times = {n: [] for n, _ in vs}
+        reps = 1 if a.profile else a.reps
+        if not a.profile:
+            # one untimed launch: the first launch on fresh buffers runs slow
+            pa.attn_fwd(q, k, v, o, causal=causal, scale=scale, mapping=vs[0][1], stream=stream)
+            torch.cuda.synchronize()
+        for _ in range(reps):
+            for name, m in vs:
+                flush.zero_()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                pa.attn_fwd(q, k, v, o, causal=causal, scale=scale, mapping=m, stream=stream)
+                e1.record(stream)
+                if a.profile:
+                    manifest.append({"config": c, "variant": name})
+                torch.cuda.synchronize()
+                times[name].append(e0.elapsed_time(e1))
+        f = flops(c, causal)
+        rec = {"family": a.family, "causal": causal, **c, "d": D,
+               "ms": {n: round(statistics.median(t), 4) for n, t in times.items()},
+               "tflops": {n: round(f / statistics.median(t) / 1e9, 1) for n, t in times.items()}}
+        line = json.dumps(rec)
+        print(line, flush=True)
+        if out:
+            out.write(line + "\n")
+            out.flush()
+        del q, k, v, o
+        torch.cuda.empty_cache()
+    if a.profile and a.manifest:
+        with open(a.manifest, "w") as fm:
+            json.dump(manifest, fm)
+
+
+# ------------------------------------------------------------------ summary
+
+
+def _variant_of(kernel_name: str):
+    from paper_2511_02132_amd.rocprof_counters import variant_of
+
+    return variant_of(kernel_name)
+
+
+def l2_by_launch(counters_dir: str, manifest_path: str):
+    """{(B, Hq, Hkv, S, variant): l2 hit rate} from a --profile run under rocprofv3 --pmc."""
+    rows = {}
+    with open(os.path.join(counters_dir, "run_counter_collection.csv")) as f:
+        for r in csv.DictReader(f):
+            if _variant_of(r["Kernel_Name"]) is None:
+                continue
+            d = rows.setdefault(int(r["Dispatch_Id"]), {"variant": _variant_of(r["Kernel_Name"])})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    launches = [rows[k] for k in sorted(rows)]
+    manifest = json.load(open(manifest_path))
+    if len(launches) != len(manifest):
+        raise ValueError("%d attention dispatches in the counters, %d in the manifest"
+                         % (len(launches), len(manifest)))
+    out = {}
+    for rec, m in zip(launches, manifest):
+        if rec["variant"] != m["variant"]:
+            raise ValueError("launch order differs from the manifest")
+        c = m["config"]
+        hit, miss = rec.get("TCC_HIT", 0.0), rec.get("TCC_MISS", 0.0)
+        out[(c["B"], c["Hq"], c["Hkv"], c["S"], m["variant"])] = hit / max(hit + miss, 1.0)
+    return out
+
+
+def summarise(a):
+    recs = {}
+    for path in a.timing:   # a later file's record of a configuration replaces an earlier one
+        with open(path) as f:
+            for x in f:
+                if x.strip():
+                    r = json.loads(x)
+                    recs[(r["S"], r["B"], r["Hq"], r["Hkv"])] = r
+    recs = [recs[k] for k in sorted(recs)]
+    l2 = l2_by_launch(a.counters, a.manifest) if a.counters else {}
+    causal = recs[0]["causal"] if recs else True
+    names = [n for n, _ in variants(causal)]
+    short = {"naive_block_first": "NBF", "naive_head_first": "NHF", "swizzled_head_first": "SHF",
+             "swizzled_block_first": "SBF"}
+
+    def sh(n):
+        base, _, extra = n.partition("+")
+        return short[base] + ("+hf" if extra else "")
+
+    base = "swizzled_head_first" + ("+heavy_first" if causal else "")
+    lines = ["# Mapping sweep: %s, d=128, %s" % (recs[0]["family"].upper() if recs else "?",
+                                                  "causal" if causal else "non-causal"), ""]
+    lines += ["Each cell: TFLOP/s (median of the interleaved, L2+MALL-flushed launches), then "
+              "relative to %s." % base]
+    if l2:
+        lines += ["Second table: L2 hit rate of one launch per variant (rocprofv3 TCC_HIT / "
+                  "(TCC_HIT + TCC_MISS))."]
+    lines += ["", "Variants: NBF naive block-first, NHF naive head-first, SHF swizzled head-first "
+              "(the method), SBF swizzled block-first; +hf = heavy-first block order.", ""]
+    if a.cmd:
+        lines += ["Commands:", "", "```", a.cmd, "```", ""]
+    hdr = "| S | B | Hq/Hkv | " + " | ".join(sh(n) for n in names) + " |"
+    lines += [hdr, "|" + "---|" * (3 + len(names))]
+    for r in recs:
+        ref = r["tflops"][base]
+        cells = ["%.0f (%.2f)" % (r["tflops"][n], r["tflops"][n] / ref) for n in names]
+        lines.append("| %dK | %d | %d/%d | %s |" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"],
+                                                   " | ".join(cells)))
+    if l2:
+        lines += ["", hdr, "|" + "---|" * (3 + len(names))]
+        for r in recs:
+            cells = []
+            for n in names:
+                h = l2.get((r["B"], r["Hq"], r["Hkv"], r["S"], n))
+                cells.append("-" if h is None else "%.1f%%" % (100 * h))
+            lines.append("| %dK | %d | %d/%d | %s |" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"],
+                                                       " | ".join(cells)))
+    # geometric-mean speed relative to the method, per variant
+    import math
+
+    lines += ["", "Geometric mean over the configurations, relative to %s:" % base, ""]
+    for n in names:
+        g = math.exp(sum(math.log(r["tflops"][n] / r["tflops"][base]) for r in recs) / len(recs))
+        lines.append("- %s: %.3f" % (n, g))
+    text = "\n".join(lines) + "\n"
+    if a.out:
+        with open(a.out, "w") as f:
+            f.write(text)
+    print(text)
+
+
+def main(argv=None):
+    a = parse(argv)
+    if a.summarise:
+        summarise(a)
+    else:
+        run(a)
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -21,7 +21,7 @@ from oracle import mapping as mp
 pytestmark = pytest.mark.gpu
 
 # the three mappings, each with the paper's block order and with heavy-first order
-ALL_MAPPINGS = [m | f for m in (0, 1, 2) for f in (0, 0x10)]
+ALL_MAPPINGS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)]
 
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3

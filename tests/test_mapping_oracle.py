@@ -11,7 +11,10 @@ What ties the enumeration (oracle/mapping.py) to the paper:
   * the caption example of Sections 3.2/3.3 (8 heads, 128 row blocks, 4 XCDs)
     from tests/golden/caption_example.json;
   * "one ACC at a time" (Section 3.3) for every shape whose ACC count is a
-    multiple of NX, including the GQA grouping of Section 3.1.
+    multiple of NX, including the GQA grouping of Section 3.1;
+  * swizzled block-first (Section 3.2) keeps the block-major order, puts each
+    GQA group on one XCD when the group count equals NX, serves Hq/NX heads
+    per row block on each XCD for MHA, and is naive block-first when NX = 1.
 Planted mistakes in the enumeration (monkeypatched) must fail a pin.
 """
 
@@ -96,6 +99,14 @@ def pin_caption_example(m):
     # the illustration puts heads {2x, 2x+1} on XCD x
     for x in range(NX):
         assert sorted(set(seqs[x])) == [2 * x, 2 * x + 1]
+    # swizzled block-first: block-major, and (4 groups of 2 heads) XCD x serves
+    # heads {2x, 2x+1} of every row block
+    cs = c["swizzled_block_first"]
+    t = _table(m, mp.SWIZZLED_BLOCK_FIRST, B, Hq, NB, NX)
+    assert np.all(np.diff(t[:, 2]) >= 0)
+    per = cs["heads_per_xcd_per_block"]
+    for w in range(N):
+        assert t[w][1] // per == m.xcd_of(w, NX)
 
 
 def pin_one_acc_at_a_time(m):
@@ -123,6 +134,28 @@ def pin_gqa_groups_on_one_xcd(m):
         assert hq // (Hq // Hkv) == m.xcd_of(wid, NX)
 
 
+def pin_swizzled_block_first(m):
+    """Section 3.2: block-first order; GQA groups co-located when Hkv == NX."""
+    for (B, Hq, Hkv, NB, NX) in [(1, 64, 8, 64, 8), (1, 32, 8, 16, 8), (2, 128, 8, 5, 8),
+                                 (1, 8, 4, 128, 4), (3, 16, 4, 7, 4)]:
+        N = B * Hq * NB
+        t = _table(m, mp.SWIZZLED_BLOCK_FIRST, B, Hq, NB, NX)
+        # block-major: every head of row block m (of batch b) before block m+1
+        assert np.array_equal(t[:, 0] * NB + t[:, 2], np.arange(N) // Hq)
+        for w in range(N):
+            assert t[w][1] // (Hq // Hkv) == m.xcd_of(w, NX), (B, Hq, Hkv, NB, NX, w)
+    # MHA with NX | Hq: each XCD serves the same Hq/NX heads of every row block
+    B, Hq, NB, NX = 2, 32, 6, 8
+    t = _table(m, mp.SWIZZLED_BLOCK_FIRST, B, Hq, NB, NX)
+    for x in range(NX):
+        heads = {int(t[w][1]) for w in range(x, B * Hq * NB, NX)}
+        assert heads == set(range(x * Hq // NX, (x + 1) * Hq // NX))
+    # one XCD: nothing to co-locate, the order is naive block-first
+    for (B, Hq, NB) in [(1, 5, 3), (2, 8, 4)]:
+        assert np.array_equal(_table(m, mp.SWIZZLED_BLOCK_FIRST, B, Hq, NB, 1),
+                              _table(m, mp.NAIVE_BLOCK_FIRST, B, Hq, NB, 1))
+
+
 def pin_ceil_blocks(m):
     assert m.num_row_blocks(256, 128) == 2 and m.num_row_blocks(257, 128) == 3
     assert m.num_row_blocks(1, 128) == 1 and m.grid_size(2, 3, 129, 128) == 12
@@ -148,7 +181,7 @@ def pin_heavy_first_order(m):
 
 
 PINS = [pin_heavy_first_order, pin_permutation, pin_chiplet_swizzle, pin_head_first_listing, pin_caption_example,
-        pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_ceil_blocks]
+        pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_swizzled_block_first, pin_ceil_blocks]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -164,7 +197,7 @@ def test_enumerate_matches_map_wid():
 
 def test_errors():
     with pytest.raises(ValueError):
-        mp.map_wid(3, 0, 1, 1, 1, 8)
+        mp.map_wid(4, 0, 1, 1, 1, 8)
     with pytest.raises(ValueError):
         mp.map_wid(0, 4, 1, 2, 2, 8)
 
@@ -189,6 +222,9 @@ class _Mutant:
                 b, mm, hq = me.unravel(wid, me.bf_radices(B, Hq, NB))
             elif mapping == mp.NAIVE_HEAD_FIRST:
                 b, hq, mm = me.unravel(wid, (B, Hq, NB))
+            elif mapping == mp.SWIZZLED_BLOCK_FIRST:
+                b, mm, j = me.unravel(wid, me.bf_radices(B, Hq, NB))
+                hq = me.sbf_head(j, Hq, NX)
             else:
                 b, hq, mm = me.unravel(me.swizzled_rank(wid, N, NX), (B, Hq, NB))
             if heavy_first:
@@ -197,6 +233,7 @@ class _Mutant:
         self.map_wid = overrides.get("map_wid", map_wid)
         self.__dict__.setdefault("bf_radices", lambda B, Hq, NB: (B, NB, Hq))
         self.__dict__.setdefault("reverse_block", lambda mm, NB: NB - 1 - mm)
+        self.__dict__.setdefault("sbf_head", lambda j, Hq, NX: me.swizzled_rank(j, Hq, NX))
 
 
 def _unravel_first_fastest(x, radices):
@@ -224,6 +261,10 @@ MAP_MUTANTS = {
     "block_first_head_outer": dict(bf_radices=lambda B, Hq, NB: (B, Hq, NB)),
     "floor_row_blocks": dict(num_row_blocks=lambda Sq, BM: Sq // BM),
     "heavy_first_off_by_one": dict(reverse_block=lambda mm, NB: (NB - mm) % NB),
+    "block_first_swizzle_missing": dict(sbf_head=lambda j, Hq, NX: j),
+    "block_first_swizzle_transposed": dict(
+        sbf_head=lambda j, Hq, NX: (j % (Hq // NX if Hq >= NX else 1)) * NX + j // max(Hq // NX, 1)
+        if Hq % NX == 0 else j),
 }
 
 
