@@ -103,6 +103,55 @@ int attn_fwd_probe(const void *q, const void *k, const void *v, void *o,
                    int B, int Hq, int Hkv, int Sq, int Skv, int d,
                    int causal, float scale, int mapping, int32_t *probe);
 
+/*
+ * attn_fwd_lse -- attn_fwd that also writes each row's log-sum-exp, the
+ * statistic the backward pass recomputes P from (Section 2.3.1):
+ *   lse[b][hq][i] = log sum_{j in J_i} exp(scale * <Q[b,hq,i], K[b,g,j]>)
+ * (natural log, fp32; J_i as in attn_fwd).
+ * lse : device pointer to B*Hq*Sq fp32, 4-byte aligned, owned by the caller;
+ *     must not overlap q, k, v or o.  Other arguments and behaviour as
+ *     attn_fwd.
+ */
+int attn_fwd_lse(const void *q, const void *k, const void *v, void *o, float *lse,
+                 int B, int Hq, int Hkv, int Sq, int Skv, int d,
+                 int causal, float scale, int mapping);
+
+/*
+ * attn_bwd -- attention backward pass, Section 2.3 Eq. (2) ("eq:ba"), for the
+ * forward of attn_fwd with the same (scale, causal, GQA grouping):
+ *   P_ij  = exp(scale * s_ij - lse_i),  s_ij = <Q_i, K_j>
+ *   dV_j  = sum_i P_ij dO_i                        (dV = P^T dO)
+ *   dP_ij = <dO_i, V_j>                             (dP = dO V^T)
+ *   dS_ij = P_ij (dP_ij - D_i), D_i = <dO_i, O_i>   (dS = dsoftmax(dP))
+ *   dQ_i  = scale * sum_j dS_ij K_j                 (dQ = dS K)
+ *   dK_j  = scale * sum_i dS_ij Q_i                 (dK = dS^T Q)
+ * summed over the query heads of a group for dK and dV (GQA), with i, j over
+ * the same (causal) pairs as the forward.
+ *
+ * q, k, v : the forward's inputs (layouts as attn_fwd).
+ * o : the forward's output, bf16 [B][Hq][Sq][d].
+ * dout : dL/dO, bf16 [B][Hq][Sq][d].
+ * lse : the forward's row log-sum-exp (attn_fwd_lse), fp32 [B][Hq][Sq].
+ * delta : workspace, fp32 [B][Hq][Sq], 4-byte aligned; overwritten with D.
+ * dq : output, bf16 [B][Hq][Sq][d].   dk, dv : outputs, bf16 [B][Hkv][Skv][d].
+ *     Every element of dq, dk and dv is written.
+ * d : 128 only (ATTN_ERR_UNSUPPORTED otherwise).
+ * mapping : as attn_fwd.  The dQ kernel decodes its workgroups over
+ *     (b, hq, row block of 128) and the dK/dV kernel over (b, K/V head, key
+ *     block of 128) with that mapping; ATTN_ORDER_HEAVY_FIRST reverses the row
+ *     blocks of the dQ kernel (the dK/dV kernel's natural order already starts
+ *     with the most expensive causal block).  The result is bitwise the same
+ *     for every mapping.
+ *
+ * Tensor pointers must be 16-byte aligned and the outputs and the workspace
+ * must not overlap any input or each other (ATTN_ERR_ALIGN / ATTN_ERR_ALIAS).
+ * Ownership, streams and asynchrony as attn_fwd.
+ */
+int attn_bwd(const void *q, const void *k, const void *v, const void *o, const void *dout,
+             const float *lse, float *delta, void *dq, void *dk, void *dv,
+             int B, int Hq, int Hkv, int Sq, int Skv, int d,
+             int causal, float scale, int mapping);
+
 /* Number of workgroups attn_fwd launches: B * Hq * ceil(Sq / attn_block_m(d)),
  * or a negative ATTN_ERR_* code for an invalid shape. */
 int64_t attn_grid_size(int B, int Hq, int Sq, int d);

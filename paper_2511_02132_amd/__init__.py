@@ -1,4 +1,4 @@
-"""Python binding of libattn_numa.so: NUMA-aware fused attention forward on MI355X.
+"""Python binding of libattn_numa.so: NUMA-aware fused attention on MI355X.
 
 Argument marshalling only.  Every step of the computation runs in the HIP
 kernels of ``csrc/``; there is no CPU fallback, and a missing library is an
@@ -6,6 +6,8 @@ error.  Torch provides device memory and streams.
 
     from paper_2511_02132_amd import attn_fwd, SWIZZLED_HEAD_FIRST
     o = attn_fwd(q, k, v, causal=True, mapping=SWIZZLED_HEAD_FIRST)
+    o, lse = attn_fwd_lse(q, k, v, causal=True)            # training forward
+    dq, dk, dv = attn_bwd(q, k, v, o, do, lse, causal=True)  # d = 128
 
 q: [B, Hq, Sq, d], k/v: [B, Hkv, Skv, d], bf16, contiguous, on the GPU;
 d in {64, 128}; Hq a multiple of Hkv (grouped-query attention).
@@ -42,6 +44,8 @@ SIGNATURES = {
     "attn_fwd": ([_vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_fwd_probe": ([_vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci, _vp],
                        _ci),
+    "attn_fwd_lse": ([_vp, _vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
+    "attn_bwd": ([_vp] * 10 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_grid_size": ([_ci, _ci, _ci, _ci], ctypes.c_int64),
     "attn_map_tiles": ([_ci, _ci, _ci, _ci, _ci, _ci, _i32p], _ci),
     "attn_block_m": ([_ci], _ci),
@@ -182,7 +186,63 @@ def attn_fwd_probe(q, k, v, o=None, probe=None, *, causal: bool = False,
     return o, probe
 
 
+def attn_fwd_lse(q, k, v, o=None, lse=None, *, causal: bool = False, scale: float | None = None,
+                 mapping: int = SWIZZLED_HEAD_FIRST, stream=None):
+    """attn_fwd that also returns the row log-sum-exp lse [B, Hq, Sq] fp32."""
+    import torch
+    o, (B, Hq, Hkv, Sq, Skv, d), scale = _prepare(q, k, v, o, scale, stream)
+    if lse is None:
+        lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+    _check_stat(lse, (B, Hq, Sq), q.device, "lse")
+    _check(lib().attn_fwd_lse(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                              lse.data_ptr(), B, Hq, Hkv, Sq, Skv, d, int(bool(causal)), scale,
+                              int(mapping)),
+           "attn_fwd_lse")
+    return o, lse
+
+
+def _check_stat(t, shape, device, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or tuple(t.shape) != shape \
+            or not t.is_contiguous() or t.device != device:
+        raise ValueError("%s must be a contiguous float32 GPU tensor of shape %s" % (name, shape))
+
+
+def attn_bwd(q, k, v, o, dout, lse, dq=None, dk=None, dv=None, delta=None, *,
+             causal: bool = False, scale: float | None = None,
+             mapping: int = SWIZZLED_HEAD_FIRST, stream=None):
+    """Gradients (dq, dk, dv) of attn_fwd for dL/dO = dout (bf16; d = 128).
+
+    o and lse come from attn_fwd_lse with the same causal/scale; delta is a
+    float32 [B, Hq, Sq] workspace (allocated here when not given)."""
+    import torch
+    _, (B, Hq, Hkv, Sq, Skv, d), scale = _prepare(q, k, v, o, scale, stream)
+    _shapes(q, k, v, dout)
+    if dq is None:
+        dq = torch.empty_like(q)
+    if dk is None:
+        dk = torch.empty_like(k)
+    if dv is None:
+        dv = torch.empty_like(v)
+    if delta is None:
+        delta = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+    _shapes(dq, dk, dv, dq)
+    _check_stat(lse, (B, Hq, Sq), q.device, "lse")
+    _check_stat(delta, (B, Hq, Sq), q.device, "delta")
+    _check(lib().attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                          dout.data_ptr(), lse.data_ptr(), delta.data_ptr(), dq.data_ptr(),
+                          dk.data_ptr(), dv.data_ptr(), B, Hq, Hkv, Sq, Skv, d,
+                          int(bool(causal)), scale, int(mapping)),
+           "attn_bwd")
+    return dq, dk, dv
+
+
 def attention_flops(B: int, Hq: int, Sq: int, Skv: int, d: int, causal: bool) -> float:
     """FlashAttention convention: 4*B*Hq*Sq*Skv*d, halved when causal."""
     f = 4.0 * B * Hq * Sq * Skv * d
     return f / 2 if causal else f
+
+
+def attention_bwd_flops(B: int, Hq: int, Sq: int, Skv: int, d: int, causal: bool) -> float:
+    """FlashAttention convention for the backward: 2.5x the forward (five products)."""
+    return 2.5 * attention_flops(B, Hq, Sq, Skv, d, causal)

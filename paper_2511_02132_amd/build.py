@@ -15,11 +15,12 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libattn_numa.so")
-SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_abi.cpp"]
+SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_abi.cpp"]
 ARCH = "gfx950"
 
 
-KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_device.h", "attn_internal.h"]
+KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_device.h",
+                  "attn_internal.h"]
 
 
 def kernel_source_hash() -> str:

@@ -83,9 +83,18 @@ int env_num_xcd() {
 }
 
 int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv, int Sq,
-        int Skv, int d, int causal, float scale, int mapping, int32_t *probe) {
+        int Skv, int d, int causal, float scale, int mapping, int32_t *probe, float *lse) {
     int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
     if (rc) return rc;
+    if (lse) {
+        if (((uintptr_t)lse) & 3u) return ATTN_ERR_ALIGN;
+        const int64_t lse_bytes = (int64_t)B * Hq * Sq * 4;
+        const int64_t qo_bytes = (int64_t)B * Hq * Sq * d * 2;
+        const int64_t kv_bytes = (int64_t)B * Hkv * Skv * d * 2;
+        if (overlaps(lse, lse_bytes, q, qo_bytes) || overlaps(lse, lse_bytes, k, kv_bytes) ||
+            overlaps(lse, lse_bytes, v, kv_bytes) || overlaps(lse, lse_bytes, o, qo_bytes))
+            return ATTN_ERR_ALIAS;
+    }
     const int nx = attn_num_xcd();
     if (nx < 0) return nx;
     attn::KernelArgs a;
@@ -94,6 +103,7 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.v = v;
     a.o = o;
     a.probe = probe;
+    a.lse = lse;
     a.B = B;
     a.Hq = Hq;
     a.Hkv = Hkv;
@@ -115,14 +125,76 @@ extern "C" {
 
 int attn_fwd(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv, int Sq,
              int Skv, int d, int causal, float scale, int mapping) {
-    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, nullptr);
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, nullptr, nullptr);
+}
+
+int attn_fwd_lse(const void *q, const void *k, const void *v, void *o, float *lse, int B, int Hq,
+                 int Hkv, int Sq, int Skv, int d, int causal, float scale, int mapping) {
+    if (!lse) return ATTN_ERR_NULL;
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, nullptr, lse);
+}
+
+int attn_bwd(const void *q, const void *k, const void *v, const void *o, const void *dout,
+             const float *lse, float *delta, void *dq, void *dk, void *dv, int B, int Hq, int Hkv,
+             int Sq, int Skv, int d, int causal, float scale, int mapping) {
+    if (!dout || !lse || !delta || !dq || !dk || !dv) return ATTN_ERR_NULL;
+    int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
+    if (rc) return rc;
+    if (d != 128) return ATTN_ERR_UNSUPPORTED;
+    if ((((uintptr_t)dout | (uintptr_t)dq | (uintptr_t)dk | (uintptr_t)dv) & 15u) ||
+        (((uintptr_t)lse | (uintptr_t)delta) & 3u))
+        return ATTN_ERR_ALIGN;
+    if ((((int64_t)Skv + 128) * d * 2) > INT32_MAX) return ATTN_ERR_SHAPE;
+    const int64_t qo = (int64_t)B * Hq * Sq * d * 2;
+    const int64_t kv = (int64_t)B * Hkv * Skv * d * 2;
+    const int64_t st = (int64_t)B * Hq * Sq * 4;
+    const void *in[6] = {q, k, v, o, dout, lse};
+    const int64_t in_bytes[6] = {qo, kv, kv, qo, qo, st};
+    void *out[4] = {dq, dk, dv, delta};
+    const int64_t out_bytes[4] = {qo, kv, kv, st};
+    for (int i = 0; i < 4; ++i) {
+        for (int j = 0; j < 6; ++j)
+            if (overlaps(out[i], out_bytes[i], in[j], in_bytes[j])) return ATTN_ERR_ALIAS;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlaps(out[i], out_bytes[i], out[j], out_bytes[j])) return ATTN_ERR_ALIAS;
+    }
+    const int nx = attn_num_xcd();
+    if (nx < 0) return nx;
+    attn::BwdArgs a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.dout = dout;
+    a.lse = lse;
+    a.delta = delta;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.Sq = Sq;
+    a.Skv = Skv;
+    a.NBQ = (Sq + 127) / 128;
+    a.NKV = (Skv + 127) / 128;
+    if ((int64_t)B * Hkv * a.NKV > INT32_MAX || (int64_t)B * Hq * a.NBQ > INT32_MAX ||
+        ((int64_t)B * Hq * Sq + 15) / 16 > INT32_MAX)
+        return ATTN_ERR_SHAPE;
+    a.NX = nx;
+    a.heavy_first = (mapping & ATTN_ORDER_HEAVY_FIRST) != 0;
+    a.scale = scale;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);
+    hipError_t e = attn::launch_attn_bwd(a, causal != 0, mapping & 0xf, t_stream);
+    if (e != hipSuccess) return hip_fail(e);
+    return ATTN_OK;
 }
 
 int attn_fwd_probe(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv,
                    int Sq, int Skv, int d, int causal, float scale, int mapping, int32_t *probe) {
     if (!probe) return ATTN_ERR_NULL;
     if (((uintptr_t)probe) & 3u) return ATTN_ERR_ALIGN;
-    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe);
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe, nullptr);
 }
 
 int64_t attn_grid_size(int B, int Hq, int Sq, int d) {

@@ -1,0 +1,495 @@
+// attn_bwd.hip -- attention backward pass for gfx950 (head dimension 128).
+//
+// Computes the gradients of Section 2.3, Eq. "eq:ba" for the forward of
+// Eq. "eq:fa" (softmax scale, GQA, optional top-left causal mask), given dO,
+// the forward output O and the forward's row log-sum-exp lse_i:
+//   P_ij  = exp(scale s_ij - lse_i)              (recomputed, never stored)
+//   dV_j  = sum_i P_ij dO_i
+//   dP_ij = <dO_i, V_j>
+//   dS_ij = P_ij (dP_ij - D_i),  D_i = <dO_i, O_i>  (= sum_j P_ij dP_ij)
+//   dQ_i  = scale sum_j dS_ij K_j
+//   dK_j  = scale sum_i dS_ij Q_i
+// in three kernels on one stream:
+//   1. D_i for every query row (vector ALU; HBM-bound);
+//   2. dK, dV: one workgroup per (batch b, K/V head g, block of 128 keys) --
+//      the FlashAttention-2 split of the backward over key blocks (Section
+//      2.3.1); it streams every query head of the group and every query tile
+//      of 32 rows through LDS, keeping the block's K and V rows in registers
+//      and dK, dV in fp32 accumulators, so a GQA group's sum needs no atomics;
+//   3. dQ: one workgroup per (b, query head, block of 128 rows), streaming
+//      K and V tiles of 64 keys like the forward, dQ accumulated in registers.
+// Splitting dQ from dK/dV recomputes S and dP once more, but every output is
+// written by exactly one workgroup in a fixed order: the gradients are
+// deterministic and bitwise independent of the workgroup mapping.
+//
+// Placement: both gradient kernels decode their workgroup id with the forward's
+// mappings (attn_internal.h), over (b, K/V head, key block) for dK/dV and over
+// (b, query head, row block) for dQ, so workgroups sharing Q/dO (dK/dV) or
+// K/V (dQ) stay on one XCD under swizzled head-first (Section 3.1: the
+// backward's attention compute clusters).  ATTN_ORDER_HEAVY_FIRST reverses the
+// row blocks of the dQ kernel as in the forward; the dK/dV kernel's natural
+// order already starts with the most expensive causal key block.
+//
+// MFMA forms (v_mfma_f32_32x32x16_bf16):
+//   dK/dV kernel, lanes <-> keys:
+//     S  (32 q x 32 keys)  = Q_tile K^T      A = Q rows (LDS), B = K (registers)
+//     dP (32 q x 32 keys)  = dO_tile V^T     A = dO rows (LDS), B = V (registers)
+//     dV^T (128 x 32 keys) += dO^T P         A = dO^T (transposing LDS read), B = P
+//     dK^T (128 x 32 keys) += Q^T dS         A = Q^T (transposing LDS read), B = dS
+//   dQ kernel, lanes <-> queries:
+//     S^T, dP^T (64 keys x 32 q) = K Q^T, V dO^T    A = K, V rows (LDS), B = Q, dO (registers)
+//     dQ^T (128 x 32 q) += K^T dS^T                  A = K^T (transposing LDS read), B = dS^T
+// The accumulator of S (or S^T) converted to bf16 is directly the B operand of
+// the next product; the transposing reads pick the rows in the order of the
+// accumulator's registers.  Tiles read both ways use dual_swizzle, under which
+// both access patterns are free of LDS bank conflicts.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn_device.h"
+#include "attn_internal.h"
+#include "attn_numa.h"
+
+namespace attn {
+namespace {
+
+using namespace dev;
+
+constexpr int D = 128;
+constexpr int ROW_BYTES = D * 2;
+constexpr int KSTEPS = D / 16;   // MFMA k-steps over the head dimension
+constexpr int DBLK = D / 32;     // 32-row blocks of a transposed gradient
+constexpr float kLog2e = 1.44269504088896340736f;
+
+// Chunk c (16 bytes) of row r of a tile is stored at c ^ dual_swizzle(r).
+//  * 16-byte row reads: 16 consecutive rows, one logical chunk -> the 16
+//    values of dual_swizzle over 16 consecutive rows are all distinct.
+//  * transposing reads: 4 consecutive rows x 64 bytes per 32 lanes -> the
+//    64-byte block index moves by (r & 3) and so differs between the rows.
+__device__ __forceinline__ int dual_swizzle(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+__device__ __forceinline__ uint32_t sw_off(int row, int byte) {
+    return (uint32_t)(row * ROW_BYTES + ((((byte >> 4) ^ dual_swizzle(row)) << 4) | (byte & 15)));
+}
+
+// Global source offset (within a tile) of LDS slot `slot` (16 bytes) of a
+// dual-swizzled tile: the copies fill LDS linearly and fetch the chunk that
+// belongs there.
+__device__ __forceinline__ uint32_t slot_src(int slot) {
+    const int row = slot / 16;
+    const int phys = slot % 16;
+    return (uint32_t)(row * ROW_BYTES + ((phys ^ dual_swizzle(row)) << 4));
+}
+
+// ---------------------------------------------------------------- D = <dO, O>
+
+__global__ __launch_bounds__(256) void attn_bwd_delta_kernel(const BwdArgs p) {
+    const int64_t rows = (int64_t)p.B * p.Hq * p.Sq;
+    const int64_t row = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+    const int part = threadIdx.x & 15;   // 16 bytes (8 elements) of the row
+    float acc = 0.0f;
+    if (row < rows) {
+        const int64_t off = row * ROW_BYTES + part * 16;
+        const bf16x8 x = __builtin_bit_cast(bf16x8, *(const u32x4 *)((const char *)p.o + off));
+        const bf16x8 y = __builtin_bit_cast(bf16x8, *(const u32x4 *)((const char *)p.dout + off));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc += (float)x[e] * (float)y[e];
+    }
+    acc += __shfl_xor(acc, 8, 16);
+    acc += __shfl_xor(acc, 4, 16);
+    acc += __shfl_xor(acc, 2, 16);
+    acc += __shfl_xor(acc, 1, 16);
+    if (row < rows && part == 0) p.delta[row] = acc;
+}
+
+// Per-lane offsets of the transposing read of a dual-swizzled tile: lane i of
+// 16-lane group gsel addresses row 4h + i/4 of a 16-row chunk (+8 rows for the
+// upper half of the operand) and columns 32db + 16gsel + 4(i%4).  The chunk's
+// first row (16kc + 8hi) is a multiple of 4, so the swizzle of the addressed
+// row depends only on (i/4, h, hi) and the chunk offset is an immediate.
+__device__ __forceinline__ void tr_offsets(int lane, uint32_t (&off)[DBLK][2]) {
+    const int li = lane & 15;
+    const int gsel = (lane >> 4) & 1;
+    const int h = lane >> 5;
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+#pragma unroll
+        for (int hi = 0; hi < 2; ++hi) {
+            const int row = 8 * hi + 4 * h + (li >> 2);   // row within a 16-row chunk
+            const int byte = 64 * db + 32 * gsel + 8 * (li & 3);
+            off[db][hi] = sw_off(row, byte) - 8 * hi * ROW_BYTES;
+        }
+}
+
+// A operand rows 16kc.. of a transposing read (see tr_offsets).
+__device__ __forceinline__ bf16x8 tr_operand(lds_char *base, const uint32_t (&off)[DBLK][2], int db,
+                                             int kc) {
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (lds_bf16x4 *)(base + off[db][0] + 16 * kc * ROW_BYTES));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (lds_bf16x4 *)(base + off[db][1] + (16 * kc + 8) * ROW_BYTES));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Rows of a transposed accumulator (lane holds column c; register r of block
+// db holds row 32db + 8(r/4) + 4h + r%4) scaled and stored as bf16 rows:
+// `row` of the output head, bounded by the descriptor.
+__device__ __forceinline__ void store_rows(const f32x16 (&acc)[DBLK], float s,
+                                           __amdgpu_buffer_rsrc_t r, int row, int h) {
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const f32x4 v4 = {acc[db][4 * j + 0] * s, acc[db][4 * j + 1] * s,
+                              acc[db][4 * j + 2] * s, acc[db][4 * j + 3] * s};
+            const bf16x4 b4 = __builtin_convertvector(v4, bf16x4);
+            const uint32_t off = (uint32_t)(row * D + 32 * db + 8 * j + 4 * h) * 2u;
+            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, b4), r, (int)off, 0, 0);
+        }
+    }
+}
+
+// ---------------------------------------------------------------- dK, dV
+
+constexpr int kKeysPerWg = 128;
+constexpr int kQTile = 32;
+
+template <bool CAUSAL, int MAPPING>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(const BwdArgs p) {
+    constexpr int BQ = kQTile;
+    constexpr int TILE = BQ * ROW_BYTES;          // 8 KiB: Q or dO rows of one tile
+    constexpr int STAT = 1024;                     // 32 fp32 row statistics (one 64-lane copy)
+    constexpr int STAGE = 2 * TILE + 2 * STAT;     // Q, dO, lse, D
+    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+    lds_char *const lds = (lds_char *)smem;
+    const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = lane & 31;
+    const int h = lane >> 5;
+
+    // (b, K/V head g, key block n)
+    const Tile t = map_wid(MAPPING, false, blockIdx.x, p.B, p.Hkv, p.NKV, p.NX);
+    const int Gs = p.Hq / p.Hkv;
+    const int k0 = t.m * kKeysPerWg;
+    const int kw0 = k0 + 32 * w;
+    const int my_key = kw0 + c;
+
+    const int64_t kv_head = ((int64_t)t.b * p.Hkv + t.hq) * p.Skv * D;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)p.k + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)p.v + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
+    // K, V rows of this wave as B operands: lane holds key my_key, columns 16kk + 8h .. +7.
+    bf16x8 kreg[KSTEPS], vreg[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) {
+        const uint32_t off = (uint32_t)(my_key * D + 16 * kk + 8 * h) * 2u;
+        kreg[kk] = __builtin_bit_cast(bf16x8, load16(rk, off));
+        vreg[kk] = __builtin_bit_cast(bf16x8, load16(rv, off));
+    }
+
+    // Query tiles: every query head of the group, rows from the block's first
+    // key on (causal) or all rows.
+    const int qt_begin = CAUSAL ? k0 / BQ : 0;
+    const int qt_end = (p.Sq + BQ - 1) / BQ;
+    const int n_qt = qt_end > qt_begin ? qt_end - qt_begin : 0;
+    const int total = Gs * n_qt;
+
+    // Copies of tile tt into stage buffer `buf`: wave w fills 1 KiB slots 2w,
+    // 2w+1 of the Q and dO tiles; wave 0 the lse rows, wave 1 the D rows (one
+    // 64-lane copy each; lanes past the 32 rows read zeros).
+    uint32_t src[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) src[i] = slot_src((2 * w + i) * 64 + lane);
+    auto copy_tile = [&](const int tt, const int buf) __attribute__((always_inline)) {
+        const int hq = t.hq * Gs + tt / n_qt;
+        const int q0 = (qt_begin + tt % n_qt) * BQ;
+        const int64_t row0 = ((int64_t)t.b * p.Hq + hq) * p.Sq + q0;
+        const uint32_t left = (uint32_t)(p.Sq - q0) * ROW_BYTES;
+        const uint32_t dst = lds_base + buf * STAGE;
+        const i32x4 dq = buffer_words((const char *)p.q + row0 * ROW_BYTES, left);
+        const i32x4 ddo = buffer_words((const char *)p.dout + row0 * ROW_BYTES, left);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            lds_copy16(dq, src[i], dst + (2 * w + i) * 1024);
+            lds_copy16(ddo, src[i], dst + TILE + (2 * w + i) * 1024);
+        }
+        const uint32_t nrows = (uint32_t)min(BQ, p.Sq - q0);
+        if (w == 0) lds_copy16(buffer_words(p.lse + row0, nrows * 4), lane * 16, dst + 2 * TILE);
+        if (w == 1)
+            lds_copy16(buffer_words(p.delta + row0, nrows * 4), lane * 16, dst + 2 * TILE + STAT);
+    };
+
+    uint32_t row_off[KSTEPS];   // A operand rows: row c, logical chunk 2kk + h
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) row_off[kk] = sw_off(c, (2 * kk + h) * 16);
+    uint32_t tro[DBLK][2];
+    tr_offsets(lane, tro);
+
+    f32x16 dvacc[DBLK], dkacc[DBLK];
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+        for (int r = 0; r < 16; ++r) dvacc[db][r] = dkacc[db][r] = 0.0f;
+    const float sl2 = p.scale_log2;
+
+    auto compute = [&](const int tt, auto buf_c) __attribute__((always_inline)) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const int q0 = (qt_begin + tt % n_qt) * BQ;
+        // Rows before the wave's first key see none of its keys (causal).
+        if (CAUSAL && q0 + BQ - 1 < kw0) return;
+        lds_char *const qb = lds + BUF * STAGE;
+        lds_char *const dob = qb + TILE;
+        lds_char *const lseb = qb + 2 * TILE;
+        lds_char *const db_ = lseb + STAT;
+
+        f32x16 sacc = {}, dpacc = {};
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk) {
+            const bf16x8 aq = *(const lds_bf16x8 *)(qb + row_off[kk]);
+            sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kreg[kk], sacc, 0, 0, 0);
+            const bf16x8 ado = *(const lds_bf16x8 *)(dob + row_off[kk]);
+            dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ado, vreg[kk], dpacc, 0, 0, 0);
+        }
+        // Register r holds query row 8(r/4) + 4h + r%4 of the tile.
+        const bool need_mask = CAUSAL && q0 < kw0 + 31;
+        f32x8 p8[2], ds8[2];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const f32x4 l4 = *(const lds_f32x4 *)(lseb + (8 * j + 4 * h) * 4);
+            const f32x4 d4 = *(const lds_f32x4 *)(db_ + (8 * j + 4 * h) * 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = 4 * j + e;
+                float pr = exp2_hw(__builtin_fmaf(sacc[r], sl2, -l4[e] * kLog2e));
+                if (need_mask && my_key > q0 + 8 * j + 4 * h + e) pr = 0.0f;
+                p8[r >> 3][r & 7] = pr;
+                ds8[r >> 3][r & 7] = pr * (dpacc[r] - d4[e]);
+            }
+        }
+        bf16x8 pb[2], dsb[2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            pb[kc] = __builtin_convertvector(p8[kc], bf16x8);
+            dsb[kc] = __builtin_convertvector(ds8[kc], bf16x8);
+        }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+#pragma unroll
+            for (int db = 0; db < DBLK; ++db) {
+                dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(dob, tro, db, kc),
+                                                                     pb[kc], dvacc[db], 0, 0, 0);
+                dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(qb, tro, db, kc),
+                                                                     dsb[kc], dkacc[db], 0, 0, 0);
+            }
+        }
+    };
+
+    if (total > 0) copy_tile(0, 0);
+    for (int tt = 0; tt < total; tt += 2) {
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (tt + 1 < total) copy_tile(tt + 1, 1);
+        compute(tt, Int<0>{});
+        if (tt + 1 < total) {
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+            __syncthreads();
+            if (tt + 2 < total) copy_tile(tt + 2, 0);
+            compute(tt + 1, Int<1>{});
+        }
+    }
+    // no copy is left in flight here: the last tile's copies were waited for
+
+    const __amdgpu_buffer_rsrc_t rdk = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((char *)p.dk + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rdv = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((char *)p.dv + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
+    store_rows(dkacc, p.scale, rdk, my_key, h);
+    store_rows(dvacc, 1.0f, rdv, my_key, h);
+}
+
+// ---------------------------------------------------------------- dQ
+
+constexpr int kRowsPerWg = 128;
+constexpr int kKeyTile = 64;
+
+template <bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(const BwdArgs p) {
+    constexpr int BN = kKeyTile;
+    constexpr int TILE = BN * ROW_BYTES;   // 16 KiB: K or V rows of one tile
+    constexpr int STAGE = 2 * TILE;
+    constexpr int IPW = TILE / 1024 / 4;   // copy instructions per wave per tile
+    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+    lds_char *const lds = (lds_char *)smem;
+    const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = lane & 31;
+    const int h = lane >> 5;
+
+    const Tile t = map_wid(MAPPING, HEAVY_FIRST, blockIdx.x, p.B, p.Hq, p.NBQ, p.NX);
+    const int g = t.hq / (p.Hq / p.Hkv);
+    const int q_wave0 = t.m * kRowsPerWg + 32 * w;
+    const int my_q = q_wave0 + c;
+
+    const int64_t q_head = ((int64_t)t.b * p.Hq + t.hq) * p.Sq;   // row index of the head's row 0
+    const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * D;
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)p.q + q_head * ROW_BYTES), 0, p.Sq * ROW_BYTES, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rdo = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)p.dout + q_head * ROW_BYTES), 0, p.Sq * ROW_BYTES, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rstat = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(p.lse + q_head), 0, p.Sq * 4, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rdelta = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(p.delta + q_head), 0, p.Sq * 4, kBufferFlags);
+    // Q and dO rows as B operands (lane: row my_q, columns 16kk + 8h .. +7);
+    // rows past Sq read zeros, and so do their statistics.
+    bf16x8 qreg[KSTEPS], doreg[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) {
+        const uint32_t off = (uint32_t)(my_q * D + 16 * kk + 8 * h) * 2u;
+        qreg[kk] = __builtin_bit_cast(bf16x8, load16(rq, off));
+        doreg[kk] = __builtin_bit_cast(bf16x8, load16(rdo, off));
+    }
+    const float lse2 = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(rstat, my_q * 4, 0, 0)) * kLog2e;
+    const float dq_d = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(rdelta, my_q * 4, 0, 0));
+
+    const int kv_end = CAUSAL ? min((t.m + 1) * kRowsPerWg, p.Skv) : p.Skv;
+    const int n_tiles = (kv_end + BN - 1) / BN;
+    const uint32_t kv_bytes = p.Skv * ROW_BYTES;
+    const uint32_t kv_lim = min(kv_bytes, (uint32_t)n_tiles * TILE);
+    uint32_t src[IPW];
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) src[i] = slot_src((w * IPW + i) * 64 + lane);
+    const char *const k_head = (const char *)p.k + kv_head * 2;
+    const char *const v_head = (const char *)p.v + kv_head * 2;
+    auto copy_tile = [&](const int n, const int buf) __attribute__((always_inline)) {
+        const uint32_t off = (uint32_t)n * TILE;
+        const uint32_t left = off < kv_lim ? kv_lim - off : 0u;
+        const i32x4 dk_ = buffer_words(k_head + (off < kv_lim ? off : 0u), left);
+        const i32x4 dv_ = buffer_words(v_head + (off < kv_lim ? off : 0u), left);
+        const uint32_t dst = lds_base + buf * STAGE;
+#pragma unroll
+        for (int i = 0; i < IPW; ++i) {
+            lds_copy16(dk_, src[i], dst + (w * IPW + i) * 1024);
+            lds_copy16(dv_, src[i], dst + TILE + (w * IPW + i) * 1024);
+        }
+    };
+
+    uint32_t row_off[KSTEPS];   // A operand rows: row c (+32 kb2), logical chunk 2kk + h
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) row_off[kk] = sw_off(c, (2 * kk + h) * 16);
+    uint32_t tro[DBLK][2];
+    tr_offsets(lane, tro);
+
+    f32x16 dqacc[DBLK];
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+        for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.0f;
+    const float sl2 = p.scale_log2;
+
+    auto compute = [&](const int n, auto buf_c) __attribute__((always_inline)) {
+        constexpr int BUF = decltype(buf_c)::value;
+        lds_char *const kb = lds + BUF * STAGE;
+        lds_char *const vb = kb + TILE;
+        f32x16 sacc[2] = {}, dpacc[2] = {};
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; ++kk) {
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2) {
+                const bf16x8 ak = *(const lds_bf16x8 *)(kb + row_off[kk] + kb2 * 32 * ROW_BYTES);
+                sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, qreg[kk], sacc[kb2], 0, 0, 0);
+                const bf16x8 av = *(const lds_bf16x8 *)(vb + row_off[kk] + kb2 * 32 * ROW_BYTES);
+                dpacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, doreg[kk], dpacc[kb2], 0, 0, 0);
+            }
+        }
+        // Register r of block kb2 holds key 32kb2 + 8(r/4) + 4h + r%4 of the tile.
+        const int key0 = n * BN;
+        const bool need_mask = CAUSAL && key0 + BN - 1 > q_wave0;
+        f32x8 ds8[4];
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float pr = exp2_hw(__builtin_fmaf(sacc[kb2][r], sl2, -lse2));
+                const int key = key0 + 32 * kb2 + 8 * (r >> 2) + 4 * h + (r & 3);
+                if (need_mask && key > my_q) pr = 0.0f;
+                ds8[2 * kb2 + (r >> 3)][r & 7] = pr * (dpacc[kb2][r] - dq_d);
+            }
+        bf16x8 dsb[4];
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) dsb[kc] = __builtin_convertvector(ds8[kc], bf16x8);
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc)
+#pragma unroll
+            for (int db = 0; db < DBLK; ++db)
+                dqacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(kb, tro, db, kc),
+                                                                     dsb[kc], dqacc[db], 0, 0, 0);
+    };
+
+    copy_tile(0, 0);
+    for (int n = 0; n < n_tiles; n += 2) {
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (n + 1 < n_tiles) copy_tile(n + 1, 1);
+        compute(n, Int<0>{});
+        if (n + 1 < n_tiles) {
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+            __syncthreads();
+            if (n + 2 < n_tiles) copy_tile(n + 2, 0);
+            compute(n + 1, Int<1>{});
+        }
+    }
+
+    const __amdgpu_buffer_rsrc_t rdq = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((char *)p.dq + q_head * ROW_BYTES), 0, p.Sq * ROW_BYTES, kBufferFlags);
+    store_rows(dqacc, p.scale, rdq, my_q, h);
+}
+
+// ---------------------------------------------------------------- launchers
+
+template <bool CAUSAL, int MAPPING>
+hipError_t launch_grads(const BwdArgs &a, hipStream_t stream) {
+    const int g_kv = a.B * a.Hkv * a.NKV;
+    const int g_q = a.B * a.Hq * a.NBQ;
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<CAUSAL, MAPPING>), dim3(g_kv), dim3(256), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.heavy_first)
+        hipLaunchKernelGGL((attn_bwd_dq_kernel<CAUSAL, MAPPING, true>), dim3(g_q), dim3(256), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((attn_bwd_dq_kernel<CAUSAL, MAPPING, false>), dim3(g_q), dim3(256), 0,
+                           stream, a);
+    return hipGetLastError();
+}
+
+template <bool CAUSAL>
+hipError_t launch_grads_mapping(const BwdArgs &a, int mapping, hipStream_t stream) {
+    switch (mapping) {
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_grads<CAUSAL, 0>(a, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_grads<CAUSAL, 1>(a, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_grads<CAUSAL, 2>(a, stream);
+        default: return launch_grads<CAUSAL, 3>(a, stream);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd(const BwdArgs &a, bool causal, int mapping, hipStream_t stream) {
+    const int64_t rows = (int64_t)a.B * a.Hq * a.Sq;
+    hipLaunchKernelGGL(attn_bwd_delta_kernel, dim3((unsigned)((rows + 15) / 16)), dim3(256), 0,
+                       stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return causal ? launch_grads_mapping<true>(a, mapping, stream)
+                  : launch_grads_mapping<false>(a, mapping, stream);
+}
+
+}  // namespace attn

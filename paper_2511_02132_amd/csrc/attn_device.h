@@ -21,6 +21,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
 
 constexpr int kThreads = 256;
 // Word 3 of a gfx9 buffer resource: 32-bit data format, raw (stride 0) access.
@@ -71,6 +72,22 @@ __device__ __forceinline__ float xor32(float x) {
 }
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float log2_hw(float x) { return __builtin_amdgcn_logf(x); }
+constexpr float kLn2 = 0.69314718055994530942f;
+
+// Row log-sum-exp (natural log of sum_j exp(scale * s_ij)) of a finished row:
+// mb = scale * log2(e) * m_ref and l = sum_j exp2(scale * log2(e) * s_ij - mb),
+// so the natural-log value is (mb + log2 l) * ln 2.  Written by lane `lane` < 32
+// (lanes l and l+32 own the same row) with a bounded store: rows past the end
+// are dropped.
+__device__ __forceinline__ void store_lse(float *lse_head, int rows, int row, int lane, float mb,
+                                          float l) {
+    if (lse_head == nullptr || lane >= 32) return;
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)lse_head, 0, rows * 4, kBufferFlags);
+    const float v = (mb + log2_hw(l)) * kLn2;
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, row * 4, 0, 0);
+}
 
 // s_waitcnt operand: vmcnt(0), expcnt and lgkmcnt not waited for.
 constexpr int kWaitVmcnt0 = 0x0f70;

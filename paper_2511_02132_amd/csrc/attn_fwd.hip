@@ -294,6 +294,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     // O = acc / l, rounded to bf16; lane holds d = 32db + 8j + 4h + 0..3 of its row.
     const float l_tot = l_run + xor32(l_run);
     const float inv = 1.0f / l_tot;
+    store_lse(p.lse == nullptr ? nullptr : p.lse + ((int64_t)t.b * p.Hq + t.hq) * p.Sq, p.Sq, my_q,
+              lane, mb, l_tot);
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
 #pragma unroll

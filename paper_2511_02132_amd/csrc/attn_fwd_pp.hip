@@ -424,7 +424,10 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     if (grp == 0) barrier_lds();
 
     // O = acc / l, rounded to bf16; lane holds d = 32db + 8j + 4h + 0..3 of its row.
-    const float inv = 1.0f / (lsum + xor32(lsum));
+    const float l_tot = lsum + xor32(lsum);
+    const float inv = 1.0f / l_tot;
+    store_lse(p.lse == nullptr ? nullptr : p.lse + ((int64_t)t.b * p.Hq + t.hq) * p.Sq, p.Sq, my_q,
+              lane, mb, l_tot);
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
 #pragma unroll

@@ -24,6 +24,7 @@ struct KernelArgs {
     const void *v;
     void *o;
     int32_t *probe;   // NULL, or 4 int32 per workgroup: b, hq, m, xcc
+    float *lse;       // NULL, or [B][Hq][Sq] fp32: log sum_j exp(scale * s_ij) per row
     int B, Hq, Hkv, Sq, Skv;
     int NB;           // ceil(Sq / block_m_for(d))
     int NX;           // XCD count used by the mapping
@@ -85,6 +86,29 @@ __host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, 
     return t;
 }
 
+// Backward-pass arguments (head dimension 128).  Tensors are BHSD contiguous:
+// q, o, dout, dq [B][Hq][Sq][128] and k, v, dk, dv [B][Hkv][Skv][128] bf16;
+// lse and delta [B][Hq][Sq] fp32 (delta is written by the first kernel).
+struct BwdArgs {
+    const void *q;
+    const void *k;
+    const void *v;
+    const void *o;
+    const void *dout;
+    const float *lse;
+    float *delta;
+    void *dq;
+    void *dk;
+    void *dv;
+    int B, Hq, Hkv, Sq, Skv;
+    int NBQ;          // ceil(Sq / 128): row blocks of the dQ kernel
+    int NKV;          // ceil(Skv / 128): key blocks of the dK/dV kernel
+    int NX;
+    int heavy_first;
+    float scale;
+    float scale_log2;
+};
+
 // Enqueue the forward kernel for head dimension d (64 or 128) and base mapping
 // 0..3 (one kernel instantiation per combination).
 hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int mapping, int grid,
@@ -92,5 +116,7 @@ hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int mappi
 // The head-dimension-128 kernel (attn_fwd_pp.hip).
 hipError_t launch_attn_fwd_d128(const KernelArgs &args, bool causal, int mapping, int grid,
                                 hipStream_t stream);
+// The backward pass (attn_bwd.hip): D, then dK/dV, then dQ, on one stream.
+hipError_t launch_attn_bwd(const BwdArgs &args, bool causal, int mapping, hipStream_t stream);
 
 }  // namespace attn

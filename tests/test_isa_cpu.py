@@ -26,7 +26,7 @@ import pytest
 
 from paper_2511_02132_amd import build as B
 
-KERNEL_FILES = ["attn_fwd.hip", "attn_fwd_pp.hip"]
+KERNEL_FILES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip"]
 
 # Instructions that read M0 implicitly on gfx9-family targets.
 IMPLICIT_M0 = re.compile(
@@ -125,8 +125,11 @@ def test_every_m0_use_is_a_guarded_lds_copy(listings, name):
 @pytest.mark.parametrize("name", KERNEL_FILES)
 def test_no_packed_fp32_and_no_scalar_writes(listings, name):
     for kname, body in _kernels(listings[name]):
-        # the parse found the kernel's real instruction stream
-        assert sum(ins.startswith("v_mfma_f32_32x32x16_bf16") for ins in body) >= 16, kname
+        # the parse found the kernel's real instruction stream (the D = <dO, O>
+        # kernel of the backward pass is the one without matrix-core work)
+        assert len(body) > 10, kname
+        if "delta_kernel" not in kname:
+            assert sum(ins.startswith("v_mfma_f32_32x32x16_bf16") for ins in body) >= 16, kname
         for ins in body:
             op = ins.split()[0]
             assert not PACKED_F32.match(op), (kname, ins)
@@ -142,7 +145,10 @@ def test_no_scratch_no_spills_and_resources_fit(listings, name):
         assert md.get("vgpr_spill_count", "0") == "0", md["name"]
         assert md.get("sgpr_spill_count", "0") == "0", md["name"]
         lds = int(md["group_segment_fixed_size"])
-        regs = int(md["vgpr_count"]) + int(md.get("agpr_count", "0"))
+        # on gfx950 the count covers the unified file: architectural VGPRs
+        # (up to the accumulator offset) plus the AGPRs behind them
+        regs = int(md["vgpr_count"])
+        assert int(md.get("agpr_count", "0")) <= regs
         threads = int(md["max_flat_workgroup_size"])
         # 512 registers per lane per SIMD; a workgroup's waves spread over 4 SIMDs
         waves_per_simd = max(1, threads // 256)
