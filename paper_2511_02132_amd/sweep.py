@@ -3,6 +3,11 @@
 * MHA (Section 4.3, Table "mha_sweep"): context 8K/32K/128K x batch 1/2/4/8 x
   heads (Hq = Hkv) 8/16/32/64/128, head dimension 128.
 * GQA (Section 4.4): eight KV heads, Hq = 32/64/128, same contexts and batches.
+* Backward (Section 4.6, ``--pass bwd``): the gradient kernels of attn_bwd,
+  timed after one forward that produced O and the log-sum-exp; the paper's
+  study uses 128 heads, 8K/32K/128K and batches 1-2
+  (``--family mha --heads 128 --batches 1 2 --pass bwd``).  TFLOP/s use the
+  FlashAttention convention for the backward, 2.5x the forward's flops.
 
 Every configuration runs every mapping (four of Sections 3.2-3.3, each with
 and without the heavy-first block order when causal), interleaved within a
@@ -27,6 +32,7 @@ import argparse
 import csv
 import json
 import os
+import re
 import statistics
 import sys
 
@@ -71,6 +77,7 @@ def parse(argv=None):
     p.add_argument("--heads", type=int, nargs="+", default=None,
                    help="query heads (default: the paper's list for the family)")
     p.add_argument("--non-causal", action="store_true")
+    p.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd")
     p.add_argument("--reps", type=int, default=2)
     p.add_argument("--json", default=None, help="append one JSON line per configuration")
     p.add_argument("--profile", action="store_true")
@@ -111,9 +118,21 @@ def run(a):
         scale = 1.0 / D ** 0.5
         times = {n: [] for n, _ in vs}
         reps = 1 if a.profile else a.reps
+        if a.which == "bwd":
+            do = torch.randn(shape_q, generator=gen, device=dev, dtype=torch.bfloat16)
+            o, lse = pa.attn_fwd_lse(q, k, v, o, causal=causal, scale=scale, stream=stream)
+            grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
+                     torch.empty((c["B"], c["Hq"], c["S"]), dtype=torch.float32, device=dev))
+
+        def launch(m):
+            if a.which == "bwd":
+                pa.attn_bwd(q, k, v, o, do, lse, *grads, causal=causal, scale=scale, mapping=m,
+                            stream=stream)
+            else:
+                pa.attn_fwd(q, k, v, o, causal=causal, scale=scale, mapping=m, stream=stream)
         if not a.profile:
             # one untimed launch: the first launch on fresh buffers runs slow
-            pa.attn_fwd(q, k, v, o, causal=causal, scale=scale, mapping=vs[0][1], stream=stream)
+            launch(vs[0][1])
             torch.cuda.synchronize()
         for _ in range(reps):
             for name, m in vs:
@@ -121,14 +140,14 @@ def run(a):
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-                pa.attn_fwd(q, k, v, o, causal=causal, scale=scale, mapping=m, stream=stream)
+                launch(m)
                 e1.record(stream)
                 if a.profile:
                     manifest.append({"config": c, "variant": name})
                 torch.cuda.synchronize()
                 times[name].append(e0.elapsed_time(e1))
-        f = flops(c, causal)
-        rec = {"family": a.family, "causal": causal, **c, "d": D,
+        f = flops(c, causal) * (2.5 if a.which == "bwd" else 1.0)
+        rec = {"family": a.family, "pass": a.which, "causal": causal, **c, "d": D,
                "ms": {n: round(statistics.median(t), 4) for n, t in times.items()},
                "tflops": {n: round(f / statistics.median(t) / 1e9, 1) for n, t in times.items()}}
         line = json.dumps(rec)
@@ -137,6 +156,8 @@ def run(a):
             out.write(line + "\n")
             out.flush()
         del q, k, v, o
+        if a.which == "bwd":
+            del do, lse, grads
         torch.cuda.empty_cache()
     if a.profile and a.manifest:
         with open(a.manifest, "w") as fm:
@@ -152,19 +173,48 @@ def _variant_of(kernel_name: str):
     return variant_of(kernel_name)
 
 
+# gradient kernels: attn_bwd_dkdv_kernel<causal, mapping>, attn_bwd_dq_kernel<causal, mapping, heavy>
+BWD_RE = re.compile(r"attn_bwd_(dkdv|dq)_kernel<(true|false), (\d)(?:, (true|false))?>")
+
+
 def l2_by_launch(counters_dir: str, manifest_path: str):
-    """{(B, Hq, Hkv, S, variant): l2 hit rate} from a --profile run under rocprofv3 --pmc."""
+    """{(B, Hq, Hkv, S, variant): l2 hit rate} from a --profile run under rocprofv3 --pmc.
+
+    For the backward, one manifest entry is one attn_bwd call: its dK/dV and
+    dQ dispatches are summed (the D kernel is the same for every mapping)."""
     rows = {}
     with open(os.path.join(counters_dir, "run_counter_collection.csv")) as f:
         for r in csv.DictReader(f):
-            if _variant_of(r["Kernel_Name"]) is None:
-                continue
-            d = rows.setdefault(int(r["Dispatch_Id"]), {"variant": _variant_of(r["Kernel_Name"])})
+            name = r["Kernel_Name"]
+            v = _variant_of(name)
+            kind = "fwd"
+            if v is None:
+                m = BWD_RE.search(name)
+                if m is None:
+                    continue
+                kind = m.group(1)
+                v = MAPPING_NAMES[int(m.group(3))] + ("+heavy_first" if m.group(4) == "true" else "")
+            d = rows.setdefault(int(r["Dispatch_Id"]), {"variant": v, "kind": kind})
             d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
     launches = [rows[k] for k in sorted(rows)]
     manifest = json.load(open(manifest_path))
+    if any(rec["kind"] == "dkdv" for rec in launches):
+        # backward run: drop the forward that made O and lse, and pair each dQ
+        # dispatch with the dK/dV dispatch before it
+        merged = []
+        for rec in launches:
+            if rec["kind"] == "fwd":
+                continue
+            if rec["kind"] == "dkdv":
+                merged.append(dict(rec))
+            else:
+                prev = merged[-1]
+                for key in ("TCC_HIT", "TCC_MISS"):
+                    prev[key] = prev.get(key, 0.0) + rec.get(key, 0.0)
+                prev["variant"] = rec["variant"]   # the dQ kernel carries the order flag
+        launches = merged
     if len(launches) != len(manifest):
-        raise ValueError("%d attention dispatches in the counters, %d in the manifest"
+        raise ValueError("%d attention launches in the counters, %d in the manifest"
                          % (len(launches), len(manifest)))
     out = {}
     for rec, m in zip(launches, manifest):
@@ -196,8 +246,13 @@ def summarise(a):
         return short[base] + ("+hf" if extra else "")
 
     base = "swizzled_head_first" + ("+heavy_first" if causal else "")
-    lines = ["# Mapping sweep: %s, d=128, %s" % (recs[0]["family"].upper() if recs else "?",
-                                                  "causal" if causal else "non-causal"), ""]
+    which = recs[0].get("pass", "fwd") if recs else "fwd"
+    lines = ["# Mapping sweep: %s %s, d=128, %s" % (
+        recs[0]["family"].upper() if recs else "?", "backward" if which == "bwd" else "forward",
+        "causal" if causal else "non-causal"), ""]
+    if which == "bwd":
+        lines += ["TFLOP/s of the gradient kernels (D, dK/dV, dQ) in the FlashAttention "
+                  "convention: 2.5x the forward's 4*B*Hq*S*S*d (halved when causal).", ""]
     lines += ["Each cell: TFLOP/s (median of the interleaved, L2+MALL-flushed launches), then "
               "relative to %s." % base]
     if l2:
