@@ -2,9 +2,10 @@
 
 A step is one attn_fwd call over the whole workload (default: MHA, B=1, H=32,
 S=8192, d=128, causal -- an 8B-class decoder layer) with the swizzled
-head-first mapping (for a causal mask with the heavy-first block order, which
-keeps every head on its XCD), inputs already resident in HBM.  Prints ONE JSON
-line:
+head-first mapping -- under a causal mask with two dispatch-order options that
+keep every head on its XCD: heavy-first blocks, and block-major order across
+the heads of each XCD's piece (so the four WGs an XCD receives at a time cost
+the same) -- inputs already resident in HBM.  Prints ONE JSON line:
 
   value       attention TFLOP/s (FlashAttention flop convention) of the timed
               K back-to-back steps
@@ -15,8 +16,9 @@ line:
               WRITE_SIZE (scaled by a copy kernel of known size), read from
               the committed counter summary when it was taken on this kernel
               source, else null
-  per_mapping TFLOP/s of all four mappings (and, for causal workloads, each
-              with the heavy-first block order), interleaved, cold (L2 and MALL
+  per_mapping TFLOP/s of all four mappings (for causal workloads also each
+              with the heavy-first block order) and of swizzled head-first with
+              block-major order inside each XCD, interleaved, cold (L2 and MALL
               flushed before every launch) and warm, median over reps, plus the
               L2 hit rate from the counter summary
   cpu_baseline  the fp64 CPU oracle on a time-bounded sample of the same
@@ -41,19 +43,12 @@ DEFAULT_WORKLOAD = "mha_b1_h32_s8192_d128_causal"
 METRIC = "attention fwd TFLOP/s (% of bf16 MFMA peak) + L2 hit rate, per mapping"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
-                 "swizzled_block_first"]
-HEAVY_FIRST = 0x10
 
 
 def variants(causal: bool):
     """(name, mapping value) pairs measured per mapping."""
-    out = [(n, i) for i, n in enumerate(MAPPING_NAMES)]
-    if causal:
-        out += [(n + "+heavy_first", i | HEAVY_FIRST) for i, n in enumerate(MAPPING_NAMES)]
-    return out
-
-
+    import paper_2511_02132_amd as pa
+    return pa.variants(causal)
 
 
 def kernel_source_hash() -> str:
@@ -138,8 +133,8 @@ def main():
         return
 
     # ---- headline: K back-to-back steps of the method (swizzled head-first)
-    mapping = pa.SWIZZLED_HEAD_FIRST | (HEAVY_FIRST if causal else 0)
-    headline_name = "swizzled_head_first" + ("+heavy_first" if causal else "")
+    mapping = pa.method_variant(causal)
+    headline_name = pa.variant_name(mapping)
     for _ in range(args.warmup):
         step(mapping)
     torch.cuda.synchronize()

@@ -46,7 +46,16 @@ enum {
      * K/V tiles, the expensive blocks start first and the tail shrinks.  Not
      * part of the paper's mappings (Sections 3.2, 3.3), which dispatch blocks
      * in increasing order. */
-    ATTN_ORDER_HEAVY_FIRST = 0x10
+    ATTN_ORDER_HEAVY_FIRST = 0x10,
+    /* Optional flag for ATTN_MAP_SWIZZLED_HEAD_FIRST only (ATTN_ERR_MAPPING
+     * otherwise): each XCD receives exactly the tiles it gets without the
+     * flag, but when its contiguous piece of the head-major order is made of
+     * whole heads, it dispatches them block-major across those heads.  MI355X
+     * hands an XCD its workgroups four at a time, one per shader engine, in
+     * order; under a causal mask block-major order makes those four equally
+     * expensive (measured: head-major order left one shader engine with 9%
+     * more work).  Not part of the paper's mappings. */
+    ATTN_ORDER_XCD_BLOCK_MAJOR = 0x20
 };
 
 enum {
@@ -80,7 +89,8 @@ enum {
  *     with bf16 inputs, fp32 accumulation and bf16 rounding (RNE) of P and O.
  * mapping : one of ATTN_MAP_NAIVE_BLOCK_FIRST, ATTN_MAP_NAIVE_HEAD_FIRST,
  *     ATTN_MAP_SWIZZLED_HEAD_FIRST, ATTN_MAP_SWIZZLED_BLOCK_FIRST, optionally
- *     | ATTN_ORDER_HEAVY_FIRST.
+ *     | ATTN_ORDER_HEAVY_FIRST, and for ATTN_MAP_SWIZZLED_HEAD_FIRST optionally
+ *     | ATTN_ORDER_XCD_BLOCK_MAJOR.
  *
  * Ownership: all buffers belong to the caller; nothing is retained after the
  * call returns and nothing is allocated.  The kernel is enqueued on the stream

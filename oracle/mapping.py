@@ -43,10 +43,17 @@ The three mappings (integer ``mapping`` argument of the C ABI):
      j div NX, with qh, rh = divmod(Hq, NX).  When NX divides Hq, XCD x gets
      heads x*Hq/NX .. (x+1)*Hq/NX - 1 of every row block.
 
-Order option (not one of the paper's mappings): ``heavy_first`` replaces the
-row block m by NB-1-m after any mapping, so every (b, hq) keeps its XCD but
-each head's blocks are dispatched last-to-first.  Under a causal mask block m
-costs m+1 K/V tiles, so this starts the expensive blocks first.
+Order options (not among the paper's mappings):
+  * ``heavy_first`` replaces the row block m by NB-1-m after any mapping, so
+    every (b, hq) keeps its XCD but each head's blocks are dispatched
+    last-to-first.  Under a causal mask block m costs m+1 K/V tiles, so this
+    starts the expensive blocks first.
+  * ``xcd_block_major`` (swizzled head-first only): XCD x's piece of the
+    head-major order, when it is made of whole heads (hx of them, starting at
+    L0), is dispatched block-major: its k-th WG takes L = L0 + (k mod hx)*NB +
+    k div hx.  Same tiles per XCD, different order inside the XCD.  The MI355X
+    dispatcher hands an XCD its WGs four at a time, one per shader engine
+    (measured), so under a causal mask this makes those four equally costly.
 """
 
 from __future__ import annotations
@@ -92,18 +99,32 @@ def swizzled_rank(wid: int, N: int, NX: int) -> int:
     return x * q + min(x, r) + k
 
 
+def xcd_piece(x: int, N: int, NX: int) -> tuple:
+    """(first rank L0, length) of XCD x's contiguous piece of the XCD-major listing."""
+    q, r = divmod(N, NX)
+    return x * q + min(x, r), q + (1 if x < r else 0)
+
+
 def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
-            heavy_first: bool = False) -> tuple:
+            heavy_first: bool = False, xcd_block_major: bool = False) -> tuple:
     """(b, hq, m) that WG ``wid`` computes under ``mapping``."""
     N = B * Hq * NB
     if not 0 <= wid < N:
         raise ValueError("wid out of range")
+    if xcd_block_major and mapping != SWIZZLED_HEAD_FIRST:
+        raise ValueError("the block-major order is defined for swizzled head-first only")
     if mapping == NAIVE_BLOCK_FIRST:
         b, m, hq = unravel(wid, (B, NB, Hq))
     elif mapping == NAIVE_HEAD_FIRST:
         b, hq, m = unravel(wid, (B, Hq, NB))
     elif mapping == SWIZZLED_HEAD_FIRST:
-        b, hq, m = unravel(swizzled_rank(wid, N, NX), (B, Hq, NB))
+        L = swizzled_rank(wid, N, NX)
+        L0, n = xcd_piece(wid % NX, N, NX)
+        if xcd_block_major and L0 % NB == 0 and n % NB == 0:
+            hx = n // NB                       # whole heads in the piece
+            k = L - L0                         # position within the XCD's sequence
+            L = L0 + (k % hx) * NB + k // hx   # local head k mod hx, block k div hx
+        b, hq, m = unravel(L, (B, Hq, NB))
     elif mapping == SWIZZLED_BLOCK_FIRST:
         b, m, j = unravel(wid, (B, NB, Hq))
         hq = swizzled_rank(j, Hq, NX)
@@ -115,14 +136,20 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
 
 
 def enumerate_mapping(mapping: int, B: int, Hq: int, Sq: int, BM: int, NX: int,
-                      heavy_first: bool = False) -> np.ndarray:
+                      heavy_first: bool = False, xcd_block_major: bool = False) -> np.ndarray:
     """Array [N, 3] of (b, hq, m) for wid = 0 .. N-1 (pure-Python loop)."""
     NB = num_row_blocks(Sq, BM)
     N = B * Hq * NB
     out = np.empty((N, 3), dtype=np.int64)
     for wid in range(N):
-        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX, heavy_first)
+        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX, heavy_first, xcd_block_major)
     return out
+
+
+def split_flags(mapping_with_flags: int) -> tuple:
+    """(base mapping, heavy_first, xcd_block_major) of an ABI mapping value."""
+    return (mapping_with_flags & 0xF, bool(mapping_with_flags & 0x10),
+            bool(mapping_with_flags & 0x20))
 
 
 def acc_id(b: int, hq: int, Hq: int, Hkv: int) -> int:

@@ -27,8 +27,41 @@ SWIZZLED_HEAD_FIRST = 2
 SWIZZLED_BLOCK_FIRST = 3
 # Flag OR-ed into a mapping: dispatch each head's row blocks last-to-first.
 HEAVY_FIRST = 0x10
+# Flag for SWIZZLED_HEAD_FIRST: dispatch each XCD's piece of whole heads block-major.
+XCD_BLOCK_MAJOR = 0x20
 MAPPINGS = {"naive_block_first": NAIVE_BLOCK_FIRST, "naive_head_first": NAIVE_HEAD_FIRST,
             "swizzled_head_first": SWIZZLED_HEAD_FIRST, "swizzled_block_first": SWIZZLED_BLOCK_FIRST}
+MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
+                 "swizzled_block_first"]
+
+
+def variant_name(mapping: int) -> str:
+    """Name of a mapping value with its order flags, e.g. 'swizzled_head_first+heavy_first'."""
+    name = MAPPING_NAMES[mapping & 0xF]
+    if mapping & HEAVY_FIRST:
+        name += "+heavy_first"
+    if mapping & XCD_BLOCK_MAJOR:
+        name += "+xcd_block_major"
+    return name
+
+
+def variants(causal: bool):
+    """(name, mapping value) of every variant the measurements compare: the four
+    mappings; under a causal mask each also with the heavy-first order; and
+    swizzled head-first with the block-major order inside each XCD."""
+    vals = list(range(4)) + [SWIZZLED_HEAD_FIRST | XCD_BLOCK_MAJOR]
+    if causal:
+        vals = list(range(4)) + [m | HEAVY_FIRST for m in range(4)] + \
+            [SWIZZLED_HEAD_FIRST | HEAVY_FIRST | XCD_BLOCK_MAJOR]
+    return [(variant_name(v), v) for v in vals]
+
+
+def method_variant(causal: bool) -> int:
+    """The mapping value the headline uses: the paper's swizzled head-first
+    placement; under a causal mask with heavy-first, block-major dispatch."""
+    if causal:
+        return SWIZZLED_HEAD_FIRST | HEAVY_FIRST | XCD_BLOCK_MAJOR
+    return SWIZZLED_HEAD_FIRST
 
 ATTN_OK = 0
 ATTN_ERR = {-1: "ATTN_ERR_NULL", -2: "ATTN_ERR_SHAPE", -3: "ATTN_ERR_UNSUPPORTED",

@@ -48,8 +48,15 @@ int check_shape(int B, int Hq, int Hkv, int Sq, int Skv, int d) {
 bool valid_mapping(int mapping) {
     const int base = mapping & 0xf;
     const int flags = mapping & ~0xf;
-    return base >= ATTN_MAP_NAIVE_BLOCK_FIRST && base <= ATTN_MAP_SWIZZLED_BLOCK_FIRST &&
-           (flags & ~ATTN_ORDER_HEAVY_FIRST) == 0;
+    if (base < ATTN_MAP_NAIVE_BLOCK_FIRST || base > ATTN_MAP_SWIZZLED_BLOCK_FIRST) return false;
+    if ((flags & ~(ATTN_ORDER_HEAVY_FIRST | ATTN_ORDER_XCD_BLOCK_MAJOR)) != 0) return false;
+    // the block-major order inside an XCD's piece is defined for mapping 2 only
+    return (flags & ATTN_ORDER_XCD_BLOCK_MAJOR) == 0 || base == ATTN_MAP_SWIZZLED_HEAD_FIRST;
+}
+
+int order_bits(int mapping) {
+    return ((mapping & ATTN_ORDER_HEAVY_FIRST) ? attn::kOrderHeavyFirst : 0) |
+           ((mapping & ATTN_ORDER_XCD_BLOCK_MAJOR) ? attn::kOrderXcdBlockMajor : 0);
 }
 
 bool overlaps(const void *a, int64_t a_bytes, const void *b, int64_t b_bytes) {
@@ -111,7 +118,7 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.Skv = Skv;
     a.NB = (Sq + attn::block_m_for(d) - 1) / attn::block_m_for(d);
     a.NX = nx;
-    a.heavy_first = (mapping & ATTN_ORDER_HEAVY_FIRST) != 0;
+    a.order = order_bits(mapping);
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
     const int grid = B * Hq * a.NB;
     hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, mapping & 0xf, grid, t_stream);
@@ -182,7 +189,7 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
         ((int64_t)B * Hq * Sq + 15) / 16 > INT32_MAX)
         return ATTN_ERR_SHAPE;
     a.NX = nx;
-    a.heavy_first = (mapping & ATTN_ORDER_HEAVY_FIRST) != 0;
+    a.order = order_bits(mapping);
     a.scale = scale;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);
     hipError_t e = attn::launch_attn_bwd(a, causal != 0, mapping & 0xf, t_stream);
@@ -213,7 +220,7 @@ int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *o
     if (n > INT32_MAX) return ATTN_ERR_SHAPE;
     const int nb = (Sq + attn::block_m_for(d) - 1) / attn::block_m_for(d);
     for (int64_t wid = 0; wid < n; ++wid) {
-        const attn::Tile t = attn::map_wid(mapping & 0xf, (mapping & ATTN_ORDER_HEAVY_FIRST) != 0,
+        const attn::Tile t = attn::map_wid(mapping & 0xf, order_bits(mapping),
                                            (int)wid, B, Hq, nb, NX);
         out[3 * wid + 0] = t.b;
         out[3 * wid + 1] = t.hq;
@@ -255,7 +262,7 @@ const char *attn_strerror(int code) {
         case ATTN_ERR_NULL: return "null pointer argument";
         case ATTN_ERR_SHAPE: return "invalid shape (non-positive dimension, Hq % Hkv != 0, or size limit)";
         case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (supported: 64, 128)";
-        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST)";
+        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST, and for 2 | ATTN_ORDER_XCD_BLOCK_MAJOR)";
         case ATTN_ERR_SCALE: return "scale must be finite and > 0";
         case ATTN_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
         case ATTN_ERR_HIP: return "HIP runtime error";

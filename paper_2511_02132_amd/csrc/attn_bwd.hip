@@ -154,7 +154,7 @@ __device__ __forceinline__ void store_rows(const f32x16 (&acc)[DBLK], float s,
 constexpr int kKeysPerWg = 128;
 constexpr int kQTile = 32;
 
-template <bool CAUSAL, int MAPPING>
+template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(const BwdArgs p) {
     constexpr int BQ = kQTile;
     constexpr int TILE = BQ * ROW_BYTES;          // 8 KiB: Q or dO rows of one tile
@@ -170,8 +170,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(const BwdArgs p) 
     const int c = lane & 31;
     const int h = lane >> 5;
 
-    // (b, K/V head g, key block n)
-    const Tile t = map_wid(MAPPING, false, blockIdx.x, p.B, p.Hkv, p.NKV, p.NX);
+    // (b, K/V head g, key block n); only the block-major order bit applies
+    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hkv, p.NKV, p.NX);
     const int Gs = p.Hq / p.Hkv;
     const int k0 = t.m * kKeysPerWg;
     const int kw0 = k0 + 32 * w;
@@ -315,7 +315,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(const BwdArgs p) 
 constexpr int kRowsPerWg = 128;
 constexpr int kKeyTile = 64;
 
-template <bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
+template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(const BwdArgs p) {
     constexpr int BN = kKeyTile;
     constexpr int TILE = BN * ROW_BYTES;   // 16 KiB: K or V rows of one tile
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(const BwdArgs p) {
     const int c = lane & 31;
     const int h = lane >> 5;
 
-    const Tile t = map_wid(MAPPING, HEAVY_FIRST, blockIdx.x, p.B, p.Hq, p.NBQ, p.NX);
+    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NBQ, p.NX);
     const int g = t.hq / (p.Hq / p.Hkv);
     const int q_wave0 = t.m * kRowsPerWg + 32 * w;
     const int my_q = q_wave0 + c;
@@ -454,29 +454,39 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(const BwdArgs p) {
 
 // ---------------------------------------------------------------- launchers
 
-template <bool CAUSAL, int MAPPING>
+template <bool CAUSAL, int MAPPING, int ORDER>
 hipError_t launch_grads(const BwdArgs &a, hipStream_t stream) {
     const int g_kv = a.B * a.Hkv * a.NKV;
     const int g_q = a.B * a.Hq * a.NBQ;
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<CAUSAL, MAPPING>), dim3(g_kv), dim3(256), 0, stream, a);
+    // The dK/dV kernel's natural order already starts with the heaviest causal
+    // key block; it takes only the block-major bit.
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<CAUSAL, MAPPING, (ORDER & kOrderXcdBlockMajor)>),
+                       dim3(g_kv), dim3(256), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (a.heavy_first)
-        hipLaunchKernelGGL((attn_bwd_dq_kernel<CAUSAL, MAPPING, true>), dim3(g_q), dim3(256), 0,
-                           stream, a);
-    else
-        hipLaunchKernelGGL((attn_bwd_dq_kernel<CAUSAL, MAPPING, false>), dim3(g_q), dim3(256), 0,
-                           stream, a);
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<CAUSAL, MAPPING, ORDER>), dim3(g_q), dim3(256), 0,
+                       stream, a);
     return hipGetLastError();
+}
+
+// The block-major order inside an XCD's piece exists for mapping 2 only.
+template <bool CAUSAL, int MAPPING>
+hipError_t launch_grads_order(const BwdArgs &a, hipStream_t stream) {
+    switch (MAPPING == ATTN_MAP_SWIZZLED_HEAD_FIRST ? a.order : (a.order & kOrderHeavyFirst)) {
+        case 0: return launch_grads<CAUSAL, MAPPING, 0>(a, stream);
+        case 1: return launch_grads<CAUSAL, MAPPING, 1>(a, stream);
+        case 2: return launch_grads<CAUSAL, MAPPING, (MAPPING == 2 ? 2 : 0)>(a, stream);
+        default: return launch_grads<CAUSAL, MAPPING, (MAPPING == 2 ? 3 : 1)>(a, stream);
+    }
 }
 
 template <bool CAUSAL>
 hipError_t launch_grads_mapping(const BwdArgs &a, int mapping, hipStream_t stream) {
     switch (mapping) {
-        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_grads<CAUSAL, 0>(a, stream);
-        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_grads<CAUSAL, 1>(a, stream);
-        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_grads<CAUSAL, 2>(a, stream);
-        default: return launch_grads<CAUSAL, 3>(a, stream);
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_grads_order<CAUSAL, 0>(a, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_grads_order<CAUSAL, 1>(a, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_grads_order<CAUSAL, 2>(a, stream);
+        default: return launch_grads_order<CAUSAL, 3>(a, stream);
     }
 }
 

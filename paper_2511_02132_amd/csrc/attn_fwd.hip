@@ -58,7 +58,7 @@ namespace {
 
 using namespace dev;
 
-template <int D, bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
+template <int D, bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs p) {
     constexpr int BM = kBlockM;
     constexpr int BN = kBlockN;
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     const int c = lane & 31;   // query column of the MFMA tiles
     const int h = lane >> 5;   // which half of the 64 lanes
 
-    const Tile t = map_wid(MAPPING, HEAVY_FIRST, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
+    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
     if (p.probe != nullptr && tid == 0) {
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
@@ -309,15 +309,22 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     }
 }
 
+template <int D, bool CAUSAL, int MAPPING, int ORDER>
+hipError_t launch_order(const KernelArgs &a, int grid, hipStream_t stream) {
+    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, MAPPING, ORDER>), dim3(grid), dim3(kThreads), 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
+// The block-major order inside an XCD's piece exists for mapping 2 only.
 template <int D, bool CAUSAL, int MAPPING>
 hipError_t launch_one(const KernelArgs &a, int grid, hipStream_t stream) {
-    if (a.heavy_first)
-        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, MAPPING, true>), dim3(grid), dim3(kThreads),
-                           0, stream, a);
-    else
-        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, MAPPING, false>), dim3(grid),
-                           dim3(kThreads), 0, stream, a);
-    return hipGetLastError();
+    switch (MAPPING == ATTN_MAP_SWIZZLED_HEAD_FIRST ? a.order : (a.order & kOrderHeavyFirst)) {
+        case 0: return launch_order<D, CAUSAL, MAPPING, 0>(a, grid, stream);
+        case 1: return launch_order<D, CAUSAL, MAPPING, 1>(a, grid, stream);
+        case 2: return launch_order<D, CAUSAL, MAPPING, (MAPPING == 2 ? 2 : 0)>(a, grid, stream);
+        default: return launch_order<D, CAUSAL, MAPPING, (MAPPING == 2 ? 3 : 1)>(a, grid, stream);
+    }
 }
 
 template <int D, bool CAUSAL>

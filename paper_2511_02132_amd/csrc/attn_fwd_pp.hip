@@ -12,8 +12,8 @@
 // 4-7 (rows 128..255); both stream the same K/V tiles of 64 keys.
 //
 // Per tile j a group does two steps:
-//   E(j): softmax of S(j): mask, lazy running max, P = exp2(...), the row
-//         sums of P, P -> bf16 (vector ALU);
+//   E(j): softmax of S(j): mask, P = exp2(...) against a lazily raised
+//         reference maximum, the row sums of P, P -> bf16 (vector ALU);
 //   G(j): S(j+1) = K(j+1) Q^T and O^T += V(j)^T P(j)^T (32 MFMAs).
 // The groups run these one phase apart, phases separated by workgroup
 // barriers:
@@ -115,7 +115,7 @@ __device__ __forceinline__ void wait_copies(const int n) {
         asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
 }
 
-template <bool CAUSAL, int MAPPING, bool HEAVY_FIRST>
+template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const KernelArgs p) {
     constexpr int D = 128;
     constexpr int BM = kBlockM128;
@@ -142,7 +142,7 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     const int c = lane & 31;
     const int h = lane >> 5;
 
-    const Tile t = map_wid(MAPPING, HEAVY_FIRST, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
+    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
     if (p.probe != nullptr && tid == 0) {
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
@@ -236,8 +236,13 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
 #pragma unroll
     for (int db = 0; db < DBLK; ++db)
         for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
-    // Online-softmax state (see attn_fwd.hip): lazy reference maximum m_ref,
-    // raised only when a score exceeds it by more than 2^kLazy (exp2 domain).
+    // Online-softmax state: a reference maximum m_ref that the exponentials
+    // are taken against.  It is set from the first tile's row maximum and
+    // raised (O and l rescaled) only when a tile's exponentials sum to more
+    // than 2^24 for some lane, so the common step needs no maximum at all;
+    // any reference gives the same result in exact arithmetic, because O and l
+    // are divided by the same factor, and p <= 2^24 keeps fp32 sums far from
+    // overflow.
     float m_ref = -__builtin_inff();
     float mb = -__builtin_inff();
     // Row sum of P over this lane's keys (the lane l^32 holds the row's other
@@ -262,12 +267,32 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
                     s_cur[kb2][r] = dead ? -__builtin_inff() : s_cur[kb2][r];
                 }
         }
-        float mx = s_cur[0][0];
+        // Exponentials against the current reference and their sum over this
+        // lane's keys.  The sum shows, without a maximum over the tile, whether
+        // the reference is unset (first tile: inf/NaN) or a score exceeds it by
+        // more than 2^24 in the exp2 domain; only then is the row maximum taken,
+        // O and l rescaled and the exponentials recomputed.
+        auto exps = [&](f32x8 (&p8)[4]) __attribute__((always_inline)) {
+            float ts = 0.0f;
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
+            for (int kc = 0; kc < 4; ++kc)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kb2][r]);
-        if (__any((mx - m_ref) * sl2 > kLazy)) {
+                for (int e = 0; e < 8; ++e)
+                    p8[kc][e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
+#pragma unroll
+            for (int kc = 0; kc < 4; ++kc)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ts += p8[kc][e];
+            return ts;
+        };
+        f32x8 p8[4];
+        float tsum = exps(p8);
+        if (__any(!(tsum <= 16777216.0f))) {
+            float mx = s_cur[0][0];
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kb2][r]);
             const float m_new = fmaxf(m_ref, fmaxf(mx, xor32(mx)));
             const float alpha = exp2_hw((m_ref - m_new) * sl2);
             lsum *= alpha;
@@ -277,17 +302,11 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
                 for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
             m_ref = m_new;
             mb = m_ref * sl2;
+            tsum = exps(p8);
         }
+        lsum += tsum;
 #pragma unroll
-        for (int kc = 0; kc < 4; ++kc) {
-            f32x8 p8;
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                p8[e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
-#pragma unroll
-            for (int e = 0; e < 8; ++e) lsum += p8[e];
-            pbuf[kc] = __builtin_convertvector(p8, bf16x8);
-        }
+        for (int kc = 0; kc < 4; ++kc) pbuf[kc] = __builtin_convertvector(p8[kc], bf16x8);
 #pragma unroll
         for (int kc = 0; kc < 4; ++kc) anchor(pbuf[kc]);
     };
@@ -441,24 +460,31 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     }
 }
 
-template <bool CAUSAL, int MAPPING>
+template <bool CAUSAL, int MAPPING, int ORDER>
 hipError_t launch_pp(const KernelArgs &a, int grid, hipStream_t stream) {
-    if (a.heavy_first)
-        hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, true>), dim3(grid),
-                           dim3(kPPThreads), 0, stream, a);
-    else
-        hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, false>), dim3(grid),
-                           dim3(kPPThreads), 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, ORDER>), dim3(grid), dim3(kPPThreads),
+                       0, stream, a);
     return hipGetLastError();
+}
+
+// The block-major order inside an XCD's piece exists for mapping 2 only.
+template <bool CAUSAL, int MAPPING>
+hipError_t launch_pp_order(const KernelArgs &a, int grid, hipStream_t stream) {
+    switch (MAPPING == ATTN_MAP_SWIZZLED_HEAD_FIRST ? a.order : (a.order & kOrderHeavyFirst)) {
+        case 0: return launch_pp<CAUSAL, MAPPING, 0>(a, grid, stream);
+        case 1: return launch_pp<CAUSAL, MAPPING, 1>(a, grid, stream);
+        case 2: return launch_pp<CAUSAL, MAPPING, (MAPPING == 2 ? 2 : 0)>(a, grid, stream);
+        default: return launch_pp<CAUSAL, MAPPING, (MAPPING == 2 ? 3 : 1)>(a, grid, stream);
+    }
 }
 
 template <bool CAUSAL>
 hipError_t launch_pp_mapping(const KernelArgs &a, int mapping, int grid, hipStream_t stream) {
     switch (mapping) {
-        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_pp<CAUSAL, 0>(a, grid, stream);
-        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_pp<CAUSAL, 1>(a, grid, stream);
-        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_pp<CAUSAL, 2>(a, grid, stream);
-        default: return launch_pp<CAUSAL, 3>(a, grid, stream);
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_pp_order<CAUSAL, 0>(a, grid, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_pp_order<CAUSAL, 1>(a, grid, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_pp_order<CAUSAL, 2>(a, grid, stream);
+        default: return launch_pp_order<CAUSAL, 3>(a, grid, stream);
     }
 }
 

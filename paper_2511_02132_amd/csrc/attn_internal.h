@@ -28,13 +28,17 @@ struct KernelArgs {
     int B, Hq, Hkv, Sq, Skv;
     int NB;           // ceil(Sq / block_m_for(d))
     int NX;           // XCD count used by the mapping
-    int heavy_first;  // ATTN_ORDER_HEAVY_FIRST was set
+    int order;        // kOrder* bits of the ATTN_ORDER_* flags
     float scale_log2; // scale * log2(e): softmax evaluated with exp2
 };
 
 struct Tile {
     int b, hq, m;
 };
+
+// Order bits (from ATTN_ORDER_HEAVY_FIRST and ATTN_ORDER_XCD_BLOCK_MAJOR).
+constexpr int kOrderHeavyFirst = 1;
+constexpr int kOrderXcdBlockMajor = 2;
 
 // Workgroup id -> tile (b, hq, m) for base mapping 0..3 (ATTN_MAP_*);
 // integer only.  In the kernel the arguments are uniform, so this runs on the
@@ -48,11 +52,21 @@ struct Tile {
 //     position j takes head (j mod NX)*qh + min(j mod NX, rh) + j div NX,
 //     (qh, rh) = divmod(Hq, NX): the WGs of a row that one XCD receives carry
 //     contiguous heads, so a GQA group stays on one XCD when Hkv == NX.
-// heavy_first (ATTN_ORDER_HEAVY_FIRST) then replaces m by NB-1-m: the XCD of
-// every (b, hq) is unchanged, but each head's row blocks are dispatched from
-// the last (under a causal mask the most expensive) to the first.
-__host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, int B, int Hq,
+// Order bits:
+//  kOrderXcdBlockMajor (mapping 2 only): when XCD x's piece of the head-major
+//    order consists of whole heads (hx of them), its k-th WG takes local head
+//    k mod hx and block k div hx -- the same tiles on the same XCD, dispatched
+//    block-major across the piece's heads.  The hardware hands an XCD its WGs
+//    four at a time, one per shader engine, and dispatches in order; with
+//    block-major order those four cover one row block of four heads and cost
+//    the same under a causal mask.  Pieces that are not whole heads keep the
+//    head-major order.
+//  kOrderHeavyFirst then replaces m by NB-1-m: the XCD of every (b, hq) is
+//    unchanged, but each head's row blocks are dispatched from the last (under
+//    a causal mask the most expensive) to the first.
+__host__ __device__ inline Tile map_wid(int mapping, int order, int wid, int B, int Hq,
                                         int NB, int NX) {
+    const bool heavy_first = (order & kOrderHeavyFirst) != 0;
     Tile t;
     if (mapping == 0 || mapping == 3) {
         int j = wid % Hq;
@@ -76,7 +90,14 @@ __host__ __device__ inline Tile map_wid(int mapping, bool heavy_first, int wid, 
         const int k = wid / NX;
         const int q = N / NX;
         const int r = N % NX;
-        L = x * q + (x < r ? x : r) + k;
+        const int L0 = x * q + (x < r ? x : r);
+        const int nx = q + (x < r ? 1 : 0);
+        if ((order & kOrderXcdBlockMajor) != 0 && L0 % NB == 0 && nx % NB == 0) {
+            const int hx = nx / NB;
+            L = L0 + (k % hx) * NB + k / hx;
+        } else {
+            L = L0 + k;
+        }
     }
     t.m = L % NB;
     const int rest = L / NB;
@@ -104,7 +125,7 @@ struct BwdArgs {
     int NBQ;          // ceil(Sq / 128): row blocks of the dQ kernel
     int NKV;          // ceil(Skv / 128): key blocks of the dK/dV kernel
     int NX;
-    int heavy_first;
+    int order;        // kOrder* bits
     float scale;
     float scale_log2;
 };

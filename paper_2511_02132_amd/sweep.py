@@ -38,7 +38,6 @@ import sys
 
 MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
                  "swizzled_block_first"]
-HEAVY_FIRST = 0x10
 CONTEXTS = (8192, 32768, 131072)
 BATCHES = (1, 2, 4, 8)
 MHA_HEADS = (8, 16, 32, 64, 128)
@@ -48,10 +47,8 @@ D = 128
 
 
 def variants(causal: bool):
-    out = [(n, i) for i, n in enumerate(MAPPING_NAMES)]
-    if causal:
-        out += [(n + "+heavy_first", i | HEAVY_FIRST) for i, n in enumerate(MAPPING_NAMES)]
-    return out
+    import paper_2511_02132_amd as pa
+    return pa.variants(causal)
 
 
 def configs(family: str, contexts, batches, heads):
@@ -173,8 +170,9 @@ def _variant_of(kernel_name: str):
     return variant_of(kernel_name)
 
 
-# gradient kernels: attn_bwd_dkdv_kernel<causal, mapping>, attn_bwd_dq_kernel<causal, mapping, heavy>
-BWD_RE = re.compile(r"attn_bwd_(dkdv|dq)_kernel<(true|false), (\d)(?:, (true|false))?>")
+# gradient kernels: attn_bwd_dkdv_kernel<causal, mapping, order>, attn_bwd_dq_kernel<causal,
+# mapping, order> (the dK/dV kernel carries only the block-major bit)
+BWD_RE = re.compile(r"attn_bwd_(dkdv|dq)_kernel<(true|false), (\d), (\d)>")
 
 
 def l2_by_launch(counters_dir: str, manifest_path: str):
@@ -193,7 +191,8 @@ def l2_by_launch(counters_dir: str, manifest_path: str):
                 if m is None:
                     continue
                 kind = m.group(1)
-                v = MAPPING_NAMES[int(m.group(3))] + ("+heavy_first" if m.group(4) == "true" else "")
+                from paper_2511_02132_amd.rocprof_counters import order_suffix
+                v = MAPPING_NAMES[int(m.group(3))] + order_suffix(int(m.group(4)))
             d = rows.setdefault(int(r["Dispatch_Id"]), {"variant": v, "kind": kind})
             d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
     launches = [rows[k] for k in sorted(rows)]
@@ -211,7 +210,7 @@ def l2_by_launch(counters_dir: str, manifest_path: str):
                 prev = merged[-1]
                 for key in ("TCC_HIT", "TCC_MISS"):
                     prev[key] = prev.get(key, 0.0) + rec.get(key, 0.0)
-                prev["variant"] = rec["variant"]   # the dQ kernel carries the order flag
+                prev["variant"] = rec["variant"]   # the dQ kernel carries every order bit
         launches = merged
     if len(launches) != len(manifest):
         raise ValueError("%d attention launches in the counters, %d in the manifest"
@@ -242,10 +241,15 @@ def summarise(a):
              "swizzled_block_first": "SBF"}
 
     def sh(n):
-        base, _, extra = n.partition("+")
-        return short[base] + ("+hf" if extra else "")
+        parts = n.split("+")
+        return short[parts[0]] + ("+hf" if "heavy_first" in parts else "") + \
+            ("+bm" if "xcd_block_major" in parts else "")
 
-    base = "swizzled_head_first" + ("+heavy_first" if causal else "")
+    import paper_2511_02132_amd as pa
+    base = pa.variant_name(pa.method_variant(causal))
+    if recs and base not in recs[0]["tflops"]:   # records taken before the block-major order
+        base = "swizzled_head_first" + ("+heavy_first" if causal else "")
+    names = [n for n in names if not recs or n in recs[0]["tflops"]]
     which = recs[0].get("pass", "fwd") if recs else "fwd"
     lines = ["# Mapping sweep: %s %s, d=128, %s" % (
         recs[0]["family"].upper() if recs else "?", "backward" if which == "bwd" else "forward",
@@ -259,7 +263,8 @@ def summarise(a):
         lines += ["Second table: L2 hit rate of one launch per variant (rocprofv3 TCC_HIT / "
                   "(TCC_HIT + TCC_MISS))."]
     lines += ["", "Variants: NBF naive block-first, NHF naive head-first, SHF swizzled head-first "
-              "(the method), SBF swizzled block-first; +hf = heavy-first block order.", ""]
+              "(the method), SBF swizzled block-first; +hf = heavy-first block order, +bm = "
+              "block-major order inside each XCD's piece.", ""]
     if a.cmd:
         lines += ["Commands:", "", "```", a.cmd, "```", ""]
     hdr = "| S | B | Hq/Hkv | " + " | ".join(sh(n) for n in names) + " |"

@@ -51,8 +51,10 @@ def call(q=Q, k=K, v=V, o=O, B=1, Hq=4, Hkv=2, Sq=256, Skv=256, d=128, causal=0,
     (dict(B=0), -2), (dict(Hq=0), -2), (dict(Hkv=0), -2), (dict(Sq=0), -2), (dict(Skv=-1), -2),
     (dict(Hq=6, Hkv=4), -2), (dict(Sq=2 ** 23), -2), (dict(Skv=2 ** 23), -2),
     (dict(d=96), -3), (dict(d=256), -3), (dict(d=0), -2),
-    (dict(mapping=4), -4), (dict(mapping=-1), -4), (dict(mapping=0x20 | 2), -4),
+    (dict(mapping=4), -4), (dict(mapping=-1), -4), (dict(mapping=0x40 | 2), -4),
     (dict(mapping=0x14), -4), (dict(mapping=0xf), -4),
+    # the block-major order inside an XCD's piece exists for swizzled head-first only
+    (dict(mapping=0x20 | 0), -4), (dict(mapping=0x20 | 1), -4), (dict(mapping=0x30 | 3), -4),
     (dict(scale=float("nan")), -5), (dict(scale=float("inf")), -5), (dict(scale=0.0), -5),
     (dict(scale=-1.0), -5),
     (dict(q=Q + 8), -6), (dict(o=O + 2), -6),
@@ -105,11 +107,12 @@ MAP_SHAPES = [(1, 4, 256, 64, 8), (1, 32, 8192, 128, 8), (1, 64, 8192, 128, 8),
 @pytest.mark.parametrize("B,Hq,Sq,d,NX", MAP_SHAPES)
 def test_library_mapping_equals_oracle(B, Hq, Sq, d, NX):
     BM = pa.block_m(d)
-    for mapping in (0, 1, 2, 3):
-        for heavy in (False, True):
-            got = pa.map_tiles(mapping | (pa.HEAVY_FIRST if heavy else 0), B, Hq, Sq, d, NX)
-            want = mp.enumerate_mapping(mapping, B, Hq, Sq, BM, NX, heavy_first=heavy)
-            assert np.array_equal(got, want), (mapping, heavy)
+    for value in [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]:
+        mapping, heavy, xbm = mp.split_flags(value)
+        got = pa.map_tiles(value, B, Hq, Sq, d, NX)
+        want = mp.enumerate_mapping(mapping, B, Hq, Sq, BM, NX, heavy_first=heavy,
+                                    xcd_block_major=xbm)
+        assert np.array_equal(got, want), hex(value)
 
 
 def test_map_tiles_errors():

@@ -20,8 +20,9 @@ from oracle import mapping as mp
 
 pytestmark = pytest.mark.gpu
 
-# the three mappings, each with the paper's block order and with heavy-first order
-ALL_MAPPINGS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)]
+# the four mappings, each with the paper's block order and with heavy-first order,
+# and swizzled head-first with block-major order inside each XCD's piece
+ALL_MAPPINGS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]
 
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
@@ -68,12 +69,13 @@ def test_probe_matches_enumeration_and_dispatch(B, Hq, Hkv, S, d):
     nx = pa.num_xcd()
     BM = pa.block_m(d)
     outs = []
-    for mapping, heavy in [(m, hf) for m in mp.MAPPINGS for hf in (False, True)]:
-        flag = pa.HEAVY_FIRST if heavy else 0
-        o, probe = pa.attn_fwd_probe(q, k, v, causal=True, mapping=mapping | flag)
+    for value in ALL_MAPPINGS:
+        mapping, heavy, xbm = mp.split_flags(value)
+        o, probe = pa.attn_fwd_probe(q, k, v, causal=True, mapping=value)
         torch.cuda.synchronize()
         rec = probe.cpu().numpy()
-        want = mp.enumerate_mapping(mapping, B, Hq, S, BM, nx, heavy_first=heavy)
+        want = mp.enumerate_mapping(mapping, B, Hq, S, BM, nx, heavy_first=heavy,
+                                    xcd_block_major=xbm)
         assert np.array_equal(rec[:, :3], want), "placement differs from the enumeration"
         wid = np.arange(rec.shape[0])
         assert np.array_equal(rec[:, 3], wid % nx), "XCC_ID != wid mod NX"

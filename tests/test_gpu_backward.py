@@ -29,7 +29,7 @@ import paper_2511_02132_amd as pa
 
 pytestmark = pytest.mark.gpu
 
-ALL_MAPPINGS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)]
+ALL_MAPPINGS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]
 REL_MAX = 1e-2
 REL_MEAN = 4e-3
 LSE_ABS = 1e-4

@@ -12,6 +12,11 @@ What ties the enumeration (oracle/mapping.py) to the paper:
     from tests/golden/caption_example.json;
   * "one ACC at a time" (Section 3.3) for every shape whose ACC count is a
     multiple of NX, including the GQA grouping of Section 3.1;
+  * the block-major order inside an XCD's piece (an order option for swizzled
+    head-first) keeps every XCD's set of tiles, dispatches whole-head pieces
+    block-major so each group of four consecutive WGs of an XCD shares a row
+    block when the piece holds a multiple of four heads, and leaves other
+    pieces in head-major order;
   * swizzled block-first (Section 3.2) keeps the block-major order, puts each
     GQA group on one XCD when the group count equals NX, serves Hq/NX heads
     per row block on each XCD for MHA, and is naive block-first when NX = 1.
@@ -156,6 +161,41 @@ def pin_swizzled_block_first(m):
                               _table(m, mp.NAIVE_BLOCK_FIRST, B, Hq, NB, 1))
 
 
+def pin_xcd_block_major(m):
+    """Order option for swizzled head-first: same XCD tile sets, block-major inside."""
+    for (B, Hq, NB, NX) in SHAPES[::3] + [(1, 32, 32, 8), (1, 64, 32, 8), (8, 64, 16, 8),
+                                          (1, 16, 512, 8), (2, 12, 3, 8)]:
+        N = B * Hq * NB
+        for heavy in (False, True):
+            plain = _table(m, mp.SWIZZLED_HEAD_FIRST, B, Hq, NB, NX) if not heavy else \
+                np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, True)
+                          for w in range(N)])
+            bm = np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, heavy, True)
+                           for w in range(N)])
+            keys = (bm[:, 0] * Hq + bm[:, 1]) * NB + bm[:, 2]
+            assert np.array_equal(np.sort(keys), np.arange(N))       # a permutation
+            for x in range(NX):
+                sel = np.arange(x, N, NX)
+                assert {tuple(r) for r in plain[sel]} == {tuple(r) for r in bm[sel]}
+                L0, n = m.xcd_piece(x, N, NX)
+                seq = bm[sel]
+                if n == 0:
+                    continue
+                if L0 % NB == 0 and n % NB == 0:
+                    hx = n // NB
+                    blocks = seq[:, 2] if not heavy else NB - 1 - seq[:, 2]
+                    # block-major: block k // hx, heads of the piece in order
+                    assert np.array_equal(blocks, np.arange(n) // hx), (B, Hq, NB, NX, x)
+                    heads = seq[:, 0] * Hq + seq[:, 1]
+                    assert np.array_equal(heads - heads.min(), np.arange(n) % hx)
+                    if hx % 4 == 0:   # four consecutive WGs share a row block
+                        assert all(len(set(blocks[i:i + 4])) == 1 for i in range(0, n, 4))
+                else:
+                    assert np.array_equal(seq, plain[sel])
+    with pytest.raises(ValueError):
+        m.map_wid(mp.NAIVE_BLOCK_FIRST, 0, 1, 8, 4, 8, False, True)
+
+
 def pin_ceil_blocks(m):
     assert m.num_row_blocks(256, 128) == 2 and m.num_row_blocks(257, 128) == 3
     assert m.num_row_blocks(1, 128) == 1 and m.grid_size(2, 3, 129, 128) == 12
@@ -181,7 +221,8 @@ def pin_heavy_first_order(m):
 
 
 PINS = [pin_heavy_first_order, pin_permutation, pin_chiplet_swizzle, pin_head_first_listing, pin_caption_example,
-        pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_swizzled_block_first, pin_ceil_blocks]
+        pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_swizzled_block_first,
+        pin_xcd_block_major, pin_ceil_blocks]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -214,10 +255,12 @@ class _Mutant:
         # map_wid must see the replaced helpers
         me = self
 
-        def map_wid(mapping, wid, B, Hq, NB, NX, heavy_first=False):
+        def map_wid(mapping, wid, B, Hq, NB, NX, heavy_first=False, xcd_block_major=False):
             N = B * Hq * NB
             if not 0 <= wid < N:
                 raise ValueError("wid out of range")
+            if xcd_block_major and mapping != mp.SWIZZLED_HEAD_FIRST:
+                raise ValueError("block-major order needs swizzled head-first")
             if mapping == mp.NAIVE_BLOCK_FIRST:
                 b, mm, hq = me.unravel(wid, me.bf_radices(B, Hq, NB))
             elif mapping == mp.NAIVE_HEAD_FIRST:
@@ -226,7 +269,10 @@ class _Mutant:
                 b, mm, j = me.unravel(wid, me.bf_radices(B, Hq, NB))
                 hq = me.sbf_head(j, Hq, NX)
             else:
-                b, hq, mm = me.unravel(me.swizzled_rank(wid, N, NX), (B, Hq, NB))
+                L = me.swizzled_rank(wid, N, NX)
+                if xcd_block_major:
+                    L = me.bm_rank(L, wid % NX, N, NX, NB)
+                b, hq, mm = me.unravel(L, (B, Hq, NB))
             if heavy_first:
                 mm = me.reverse_block(mm, NB)
             return b, hq, mm
@@ -234,6 +280,32 @@ class _Mutant:
         self.__dict__.setdefault("bf_radices", lambda B, Hq, NB: (B, NB, Hq))
         self.__dict__.setdefault("reverse_block", lambda mm, NB: NB - 1 - mm)
         self.__dict__.setdefault("sbf_head", lambda j, Hq, NX: me.swizzled_rank(j, Hq, NX))
+        self.__dict__.setdefault("bm_rank", _bm_rank)
+
+
+def _bm_rank(L, x, N, NX, NB):
+    L0, n = mp.xcd_piece(x, N, NX)
+    if L0 % NB or n % NB:
+        return L
+    hx = n // NB
+    k = L - L0
+    return L0 + (k % hx) * NB + k // hx
+
+
+def _bm_rank_transposed(L, x, N, NX, NB):
+    L0, n = mp.xcd_piece(x, N, NX)
+    if L0 % NB or n % NB:
+        return L
+    hx = n // NB
+    k = L - L0
+    return L0 + (k // hx) * hx + k % hx if hx == NB else L0 + (k // hx) * NB + k % hx
+
+
+def _bm_rank_any_piece(L, x, N, NX, NB):
+    L0, n = mp.xcd_piece(x, N, NX)
+    hx = max(1, -(-n // NB))
+    k = L - L0
+    return L0 + (k % hx) * NB + k // hx
 
 
 def _unravel_first_fastest(x, radices):
@@ -262,6 +334,8 @@ MAP_MUTANTS = {
     "floor_row_blocks": dict(num_row_blocks=lambda Sq, BM: Sq // BM),
     "heavy_first_off_by_one": dict(reverse_block=lambda mm, NB: (NB - mm) % NB),
     "block_first_swizzle_missing": dict(sbf_head=lambda j, Hq, NX: j),
+    "block_major_transposed": dict(bm_rank=_bm_rank_transposed),
+    "block_major_on_partial_pieces": dict(bm_rank=_bm_rank_any_piece),
     "block_first_swizzle_transposed": dict(
         sbf_head=lambda j, Hq, NX: (j % (Hq // NX if Hq >= NX else 1)) * NX + j // max(Hq // NX, 1)
         if Hq % NX == 0 else j),
