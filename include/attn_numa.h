@@ -162,6 +162,34 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
              int B, int Hq, int Hkv, int Sq, int Skv, int d,
              int causal, float scale, int mapping);
 
+/*
+ * attn_fwd_persistent -- attn_fwd (optionally also writing lse, as
+ * attn_fwd_lse) in a persistent, dispatch-independent form (head dimension 128
+ * only): one workgroup per compute unit reads the XCD it runs on (XCC_ID) and
+ * takes tiles from a queue per XCD.  Queue x hands out the workgroup ids
+ * wid = x + NX*t, t = 0, 1, ..., i.e. exactly the tiles the round-robin
+ * dispatcher of Section 2.2 would send to XCD x under `mapping`, in the same
+ * order, so the placement no longer depends on the hardware's dispatch policy
+ * (which the paper notes may change).  A workgroup whose queue is empty takes
+ * tiles left in the other queues, so every tile is computed.  The next ticket
+ * is requested while a tile runs, hiding the gap between workgroups.
+ *
+ * queue : device pointer to ATTN_QUEUE_INTS int32, 4-byte aligned, owned by the
+ *     caller; all zero before the call (e.g. allocated zeroed once).  The last
+ *     workgroup of each launch sets it back to zero, so launches ordered on
+ *     one stream may reuse it; launches that may run concurrently need
+ *     separate queues.  Must not overlap the tensors.
+ * lse : NULL, or as attn_fwd_lse.
+ * probe : NULL, or as attn_fwd_probe (indexed by wid; xcc is the XCD that ran
+ *     the tile).
+ * Other arguments and behaviour as attn_fwd; ATTN_ERR_UNSUPPORTED for d != 128
+ * or more than 32 XCDs.  The output is bitwise that of attn_fwd.
+ */
+#define ATTN_QUEUE_INTS 64
+int attn_fwd_persistent(const void *q, const void *k, const void *v, void *o, float *lse,
+                        int32_t *queue, int32_t *probe, int B, int Hq, int Hkv, int Sq, int Skv,
+                        int d, int causal, float scale, int mapping);
+
 /* Number of workgroups attn_fwd launches: B * Hq * ceil(Sq / attn_block_m(d)),
  * or a negative ATTN_ERR_* code for an invalid shape. */
 int64_t attn_grid_size(int B, int Hq, int Sq, int d);

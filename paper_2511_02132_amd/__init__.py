@@ -78,6 +78,7 @@ SIGNATURES = {
     "attn_fwd_probe": ([_vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci, _vp],
                        _ci),
     "attn_fwd_lse": ([_vp, _vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
+    "attn_fwd_persistent": ([_vp] * 7 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_bwd": ([_vp] * 10 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_grid_size": ([_ci, _ci, _ci, _ci], ctypes.c_int64),
     "attn_map_tiles": ([_ci, _ci, _ci, _ci, _ci, _ci, _i32p], _ci),
@@ -232,6 +233,42 @@ def attn_fwd_lse(q, k, v, o=None, lse=None, *, causal: bool = False, scale: floa
                               int(mapping)),
            "attn_fwd_lse")
     return o, lse
+
+
+QUEUE_INTS = 64   # ATTN_QUEUE_INTS
+
+
+def new_queue(device):
+    """A zeroed tile-queue buffer for attn_fwd_persistent (reusable on one stream)."""
+    import torch
+    return torch.zeros(QUEUE_INTS, dtype=torch.int32, device=device)
+
+
+def attn_fwd_persistent(q, k, v, o=None, *, lse=None, queue=None, probe=None,
+                        causal: bool = False, scale: float | None = None,
+                        mapping: int = SWIZZLED_HEAD_FIRST, stream=None):
+    """attn_fwd in the persistent form (one workgroup per CU pulling tiles from
+    per-XCD queues; d = 128).  Returns o (and writes lse / probe when given)."""
+    import torch
+    o, (B, Hq, Hkv, Sq, Skv, d), scale = _prepare(q, k, v, o, scale, stream)
+    if queue is None:
+        queue = new_queue(q.device)
+    if queue.dtype != torch.int32 or queue.numel() < QUEUE_INTS or not queue.is_contiguous() \
+            or queue.device != q.device:
+        raise ValueError("queue must be a contiguous int32 GPU tensor of %d zeros" % QUEUE_INTS)
+    if lse is not None:
+        _check_stat(lse, (B, Hq, Sq), q.device, "lse")
+    if probe is not None and (probe.dtype != torch.int32 or not probe.is_contiguous()
+                              or probe.numel() < 4 * grid_size(B, Hq, Sq, d)
+                              or probe.device != q.device):
+        raise ValueError("probe must be a contiguous int32 GPU tensor with >= 4*N elements")
+    _check(lib().attn_fwd_persistent(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                     None if lse is None else lse.data_ptr(), queue.data_ptr(),
+                                     None if probe is None else probe.data_ptr(),
+                                     B, Hq, Hkv, Sq, Skv, d, int(bool(causal)), scale,
+                                     int(mapping)),
+           "attn_fwd_persistent")
+    return o
 
 
 def _check_stat(t, shape, device, name):

@@ -21,6 +21,27 @@ thread_local char t_hip_error[256] = "";
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_nx_cache[kMaxDevices];   // 0 = not yet queried
+std::atomic<int> g_cu_cache[kMaxDevices];   // compute units per device, 0 = not yet queried
+
+int hip_fail(hipError_t e);
+
+// Compute units of the current device (cached), or a negative ATTN_ERR_*.
+static_assert(ATTN_QUEUE_INTS == attn::kQueueInts && attn::kQueueDone < ATTN_QUEUE_INTS,
+              "queue layout");
+
+int num_cu() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (dev < 0 || dev >= kMaxDevices) return ATTN_ERR_UNSUPPORTED;
+    int n = g_cu_cache[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (n <= 0) return ATTN_ERR_UNSUPPORTED;
+    g_cu_cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
 
 int hip_fail(hipError_t e) {
     std::snprintf(t_hip_error, sizeof t_hip_error, "%s (%d)", hipGetErrorString(e), (int)e);
@@ -90,7 +111,8 @@ int env_num_xcd() {
 }
 
 int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv, int Sq,
-        int Skv, int d, int causal, float scale, int mapping, int32_t *probe, float *lse) {
+        int Skv, int d, int causal, float scale, int mapping, int32_t *probe, float *lse,
+        int32_t *queue = nullptr) {
     int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
     if (rc) return rc;
     if (lse) {
@@ -104,13 +126,14 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     }
     const int nx = attn_num_xcd();
     if (nx < 0) return nx;
-    attn::KernelArgs a;
+    attn::KernelArgs a{};   // every field zero (no probe, lse or queue) unless set below
     a.q = q;
     a.k = k;
     a.v = v;
     a.o = o;
     a.probe = probe;
     a.lse = lse;
+    a.queue = queue;
     a.B = B;
     a.Hq = Hq;
     a.Hkv = Hkv;
@@ -120,7 +143,13 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.NX = nx;
     a.order = order_bits(mapping);
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
-    const int grid = B * Hq * a.NB;
+    int grid = B * Hq * a.NB;
+    if (queue) {   // persistent form: one workgroup per compute unit
+        const int ncu = num_cu();
+        if (ncu < 0) return ncu;
+        if (nx > attn::kQueueMaxXcd) return ATTN_ERR_UNSUPPORTED;
+        grid = ncu;
+    }
     hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, mapping & 0xf, grid, t_stream);
     if (e != hipSuccess) return hip_fail(e);
     return ATTN_OK;
@@ -167,7 +196,7 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
     }
     const int nx = attn_num_xcd();
     if (nx < 0) return nx;
-    attn::BwdArgs a;
+    attn::BwdArgs a{};
     a.q = q;
     a.k = k;
     a.v = v;
@@ -195,6 +224,22 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
     hipError_t e = attn::launch_attn_bwd(a, causal != 0, mapping & 0xf, t_stream);
     if (e != hipSuccess) return hip_fail(e);
     return ATTN_OK;
+}
+
+int attn_fwd_persistent(const void *q, const void *k, const void *v, void *o, float *lse,
+                        int32_t *queue, int32_t *probe, int B, int Hq, int Hkv, int Sq, int Skv,
+                        int d, int causal, float scale, int mapping) {
+    if (!queue) return ATTN_ERR_NULL;
+    if (((uintptr_t)queue & 3u) || ((uintptr_t)probe & 3u)) return ATTN_ERR_ALIGN;
+    if (d != 128) return ATTN_ERR_UNSUPPORTED;
+    const int64_t qo_bytes = (int64_t)B * Hq * Sq * d * 2;
+    const int64_t kv_bytes = (int64_t)B * Hkv * Skv * d * 2;
+    const int64_t qb = (int64_t)ATTN_QUEUE_INTS * 4;
+    if (overlaps(queue, qb, q, qo_bytes) || overlaps(queue, qb, k, kv_bytes) ||
+        overlaps(queue, qb, v, kv_bytes) || overlaps(queue, qb, o, qo_bytes) ||
+        (lse && overlaps(queue, qb, lse, (int64_t)B * Hq * Sq * 4)))
+        return ATTN_ERR_ALIAS;
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe, lse, queue);
 }
 
 int attn_fwd_probe(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv,

@@ -115,8 +115,16 @@ __device__ __forceinline__ void wait_copies(const int n) {
         asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
 }
 
+// LDS of one workgroup: kStages stages of a K and a V tile (64 x 128 bf16),
+// plus the block's Q rows when kQInLds.
+constexpr int kPPLdsBytes = kStages * 2 * kBlockN * 256 + (kQInLds ? kBlockM128 * 256 : 0);
+
+// One tile (b, hq, m) of the output: the whole per-workgroup computation for
+// workgroup id `wid` (decoded by the mapping), with the LDS at `smem`.  It
+// starts and ends with every wave at the same barrier count, so a persistent
+// workgroup can run it repeatedly.
 template <bool CAUSAL, int MAPPING, int ORDER>
-__global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const KernelArgs p) {
+__device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char *smem) {
     constexpr int D = 128;
     constexpr int BM = kBlockM128;
     constexpr int BN = kBlockN;
@@ -130,8 +138,8 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     constexpr int IPW = TILE_BYTES / 1024 / WAVES;   // copy instructions per wave per tile
     static_assert(IPW * 1024 * WAVES == TILE_BYTES, "tile not divisible");
 
-    constexpr int Q_BYTES = kQInLds ? BM * ROW_BYTES : 0;   // the block's Q rows, swizzled like K
-    __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE_BYTES + Q_BYTES];
+    static_assert(kPPLdsBytes == kStages * STAGE_BYTES + (kQInLds ? BM * ROW_BYTES : 0),
+                  "LDS layout");
     lds_char *const lds = (lds_char *)smem;
     lds_char *const q_lds = lds + kStages * STAGE_BYTES;
 
@@ -142,11 +150,11 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
     const int c = lane & 31;
     const int h = lane >> 5;
 
-    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
+    const Tile t = map_wid(MAPPING, ORDER, wid, p.B, p.Hq, p.NB, p.NX);
     if (p.probe != nullptr && tid == 0) {
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
-        int32_t *rec = p.probe + 4 * (int64_t)blockIdx.x;
+        int32_t *rec = p.probe + 4 * (int64_t)wid;
         rec[0] = t.b;
         rec[1] = t.hq;
         rec[2] = t.m;
@@ -461,7 +469,78 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
 }
 
 template <bool CAUSAL, int MAPPING, int ORDER>
+__global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const KernelArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kPPLdsBytes];
+    pp_tile<CAUSAL, MAPPING, ORDER>(p, blockIdx.x, smem);
+}
+
+// Persistent form: one workgroup per CU takes tiles from per-XCD queues
+// instead of one workgroup per tile from the hardware dispatcher.  Queue x
+// hands out, in order, the workgroup ids wid = x + NX*t (t = 0, 1, ...) that
+// the dispatcher would send to XCD x, so every mapping keeps its placement,
+// whatever order the hardware starts workgroups in.  A workgroup serves the
+// queue of the XCD it runs on (XCC_ID) and, once that queue is empty, takes
+// what is left in the others (so every tile is computed even if some XCD got
+// no workgroup).  The ticket for the next tile is requested when a tile
+// starts, so its latency hides behind the tile; the launch gap between
+// workgroups (about 5 us on MI355X) disappears.
+//
+// p.queue: kQueueInts int32, zero before the launch; the last workgroup to
+// finish sets it back to zero, so launches ordered on one stream can share it.
+template <bool CAUSAL, int MAPPING, int ORDER>
+__global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_persistent_kernel(const KernelArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kPPLdsBytes];
+    __shared__ int next_wid;
+    const int N = p.B * p.Hq * p.NB;
+    const int NX = p.NX;
+    unsigned xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const int x = (int)(xcc & 0xf) % NX;
+    int *const queue = p.queue;
+    // wid of ticket t of queue qx, or -1 past its end
+    auto ticket_wid = [&](const int qx, const int tk) -> int {
+        const int n_q = (N - qx + NX - 1) / NX;
+        return tk < n_q ? qx + NX * tk : -1;
+    };
+    // Own queue first, then the others in turn.
+    auto take = [&](int first_ticket) -> int {
+        int w = ticket_wid(x, first_ticket);
+        for (int i = 1; w < 0 && i < NX; ++i) {
+            const int qx = (x + i) % NX;
+            w = ticket_wid(qx, atomicAdd(&queue[qx], 1));
+        }
+        return w;
+    };
+    if (threadIdx.x == 0) next_wid = take(atomicAdd(&queue[x], 1));
+    __syncthreads();
+    int cur = next_wid;
+    while (cur >= 0) {
+        int pending = 0;
+        if (threadIdx.x == 0) pending = atomicAdd(&queue[x], 1);   // result needed at the end
+        pp_tile<CAUSAL, MAPPING, ORDER>(p, cur, smem);
+        if (threadIdx.x == 0) next_wid = take(pending);
+        __syncthreads();
+        cur = next_wid;
+        __syncthreads();
+    }
+    // The last workgroup out clears the queue for the next launch.
+    if (threadIdx.x == 0) {
+        __threadfence();
+        if (atomicAdd(&queue[kQueueDone], 1) == (int)gridDim.x - 1) {
+            __threadfence();
+            for (int i = 0; i < NX; ++i) atomicExch(&queue[i], 0);
+            atomicExch(&queue[kQueueDone], 0);
+        }
+    }
+}
+
+template <bool CAUSAL, int MAPPING, int ORDER>
 hipError_t launch_pp(const KernelArgs &a, int grid, hipStream_t stream) {
+    if (a.queue != nullptr) {
+        hipLaunchKernelGGL((attn_fwd_pp_persistent_kernel<CAUSAL, MAPPING, ORDER>), dim3(grid),
+                           dim3(kPPThreads), 0, stream, a);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, ORDER>), dim3(grid), dim3(kPPThreads),
                        0, stream, a);
     return hipGetLastError();

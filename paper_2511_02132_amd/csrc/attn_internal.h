@@ -25,6 +25,7 @@ struct KernelArgs {
     void *o;
     int32_t *probe;   // NULL, or 4 int32 per workgroup: b, hq, m, xcc
     float *lse;       // NULL, or [B][Hq][Sq] fp32: log sum_j exp(scale * s_ij) per row
+    int *queue;       // NULL (one workgroup per tile), or the persistent form's tile queues
     int B, Hq, Hkv, Sq, Skv;
     int NB;           // ceil(Sq / block_m_for(d))
     int NX;           // XCD count used by the mapping
@@ -35,6 +36,12 @@ struct KernelArgs {
 struct Tile {
     int b, hq, m;
 };
+
+// Persistent launch: int32 words of the queue buffer -- one ticket counter per
+// XCD (at most kQueueMaxXcd) and a count of finished workgroups.
+constexpr int kQueueMaxXcd = 32;
+constexpr int kQueueDone = kQueueMaxXcd;
+constexpr int kQueueInts = 64;
 
 // Order bits (from ATTN_ORDER_HEAVY_FIRST and ATTN_ORDER_XCD_BLOCK_MAJOR).
 constexpr int kOrderHeavyFirst = 1;

@@ -1,0 +1,94 @@
+"""GPU tests of the persistent form of the forward (attn_fwd_persistent, d = 128).
+
+All calls go through the C ABI.  The persistent form must produce bitwise the
+output of attn_fwd (same per-tile arithmetic), compute every tile exactly once
+(the probe, indexed by workgroup id, equals the CPU enumeration of the
+mapping), run each tile on the XCD its queue belongs to except for tiles taken
+from another queue at the end, and leave the queue buffer zeroed so that the
+next launch on the stream can reuse it.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import attn_inputs as ai
+import paper_2511_02132_amd as pa
+from oracle import mapping as mp
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+VARIANTS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]
+SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, causal
+    (1, 32, 32, 8192, 8192, True),
+    (1, 64, 8, 2048, 2048, True),
+    (2, 12, 4, 700, 900, False),
+    (1, 3, 1, 257, 257, True),      # fewer tiles than compute units, ragged
+    (1, 1, 1, 1, 1, False),         # one tile
+]
+
+
+def _inputs(B, Hq, Hkv, Sq, Skv, seed):
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    q = torch.randn(B, Hq, Sq, 128, device=DEV, generator=g).to(torch.bfloat16)
+    k = torch.randn(B, Hkv, Skv, 128, device=DEV, generator=g).to(torch.bfloat16)
+    v = torch.randn(B, Hkv, Skv, 128, device=DEV, generator=g).to(torch.bfloat16)
+    return q, k, v
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Sq,Skv,causal", SHAPES)
+def test_persistent_equals_dispatched(B, Hq, Hkv, Sq, Skv, causal):
+    print("persistent", B, Hq, Hkv, Sq, Skv, causal, flush=True)
+    q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, 11)
+    scale = ai.default_scale(128)
+    queue = pa.new_queue(DEV)
+    nx = pa.num_xcd()
+    n = pa.grid_size(B, Hq, Sq, 128)
+    ref = pa.attn_fwd(q, k, v, causal=causal, scale=scale)
+    ref_o, ref_lse = pa.attn_fwd_lse(q, k, v, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    for value in VARIANTS:
+        mapping, heavy, xbm = mp.split_flags(value)
+        o = torch.full_like(q, float("nan"))
+        lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float32, device=DEV)
+        probe = torch.full((n, 4), -1, dtype=torch.int32, device=DEV)
+        pa.attn_fwd_persistent(q, k, v, o, lse=lse, queue=queue, probe=probe, causal=causal,
+                               scale=scale, mapping=value)
+        torch.cuda.synchronize()
+        assert torch.equal(o, ref), hex(value)
+        assert torch.equal(lse, ref_lse), hex(value)
+        assert int(queue.abs().sum()) == 0, "queue not reset by the last workgroup"
+        rec = probe.cpu().numpy()
+        want = mp.enumerate_mapping(mapping, B, Hq, Sq, pa.block_m(128), nx, heavy_first=heavy,
+                                    xcd_block_major=xbm)
+        assert np.array_equal(rec[:, :3], want), hex(value)
+        on_own_xcd = np.mean(rec[:, 3] == np.arange(n) % nx)
+        # tiles leave their XCD only when taken from another queue at the end
+        assert on_own_xcd >= (0.5 if n < 1024 else 0.9), (hex(value), on_own_xcd)
+
+
+def test_persistent_reuses_queue_back_to_back():
+    q, k, v = _inputs(1, 16, 16, 4096, 4096, 12)
+    queue = pa.new_queue(DEV)
+    ref = pa.attn_fwd(q, k, v, causal=True)
+    outs = [pa.attn_fwd_persistent(q, k, v, causal=True, queue=queue,
+                                   mapping=pa.method_variant(True)) for _ in range(5)]
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o, ref)
+    assert int(queue.abs().sum()) == 0
+
+
+def test_persistent_errors():
+    q, k, v = _inputs(1, 2, 2, 64, 64, 13)
+    with pytest.raises(pa.AttnError) as e:   # d = 64 has no persistent form
+        q64 = torch.zeros(1, 2, 64, 64, dtype=torch.bfloat16, device=DEV)
+        pa.attn_fwd_persistent(q64, q64, q64)
+    assert e.value.code == -3
+    with pytest.raises(pa.AttnError) as e:   # queue inside the output
+        o = torch.empty_like(q)
+        pa.attn_fwd_persistent(q, k, v, o, queue=o.view(torch.int32).view(-1)[:64])
+    assert e.value.code == -8
+    torch.cuda.synchronize()
