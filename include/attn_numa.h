@@ -62,7 +62,7 @@ enum {
     ATTN_OK = 0,
     ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
     ATTN_ERR_SHAPE = -2,       /* a dimension <= 0, Hq % Hkv != 0, or a size limit exceeded */
-    ATTN_ERR_UNSUPPORTED = -3, /* head dimension other than 64 or 128 */
+    ATTN_ERR_UNSUPPORTED = -3, /* head dimension other than 56, 64 or 128 (or a form that lacks it) */
     ATTN_ERR_MAPPING = -4,     /* mapping not one of ATTN_MAP_* */
     ATTN_ERR_SCALE = -5,       /* scale not finite or not > 0 */
     ATTN_ERR_ALIGN = -6,       /* a tensor pointer not 16-byte aligned */
@@ -83,8 +83,11 @@ enum {
  * v : device pointer, bf16, [B][Hkv][Skv][d] contiguous, 16-byte aligned
  * o : device pointer, bf16, [B][Hq][Sq][d] contiguous, 16-byte aligned;
  *     must not overlap q, k or v.  Every element is written.
- * d : 64 or 128.  Sq*d*2 and Skv*d*2 must each be below 2^31 bytes, and the
- *     grid B*Hq*ceil(Sq/BLOCK_M) below 2^31.
+ * d : 56, 64 or 128.  d = 56 (the DeepSeek-V3 head of Section 4.5, not a
+ *     multiple of the matrix-core step) runs the d = 64 kernel on rows padded
+ *     with zeros inside the kernel; the tensors stay 56 wide.  Sq*d*2 and
+ *     Skv*d*2 must each be below 2^31 bytes, and the grid
+ *     B*Hq*ceil(Sq/BLOCK_M) below 2^31.
  * scale : finite and > 0 (the paper uses 1/sqrt(d)); softmax is taken in fp32
  *     with bf16 inputs, fp32 accumulation and bf16 rounding (RNE) of P and O.
  * mapping : one of ATTN_MAP_NAIVE_BLOCK_FIRST, ATTN_MAP_NAIVE_HEAD_FIRST,

@@ -10,7 +10,8 @@ error.  Torch provides device memory and streams.
     dq, dk, dv = attn_bwd(q, k, v, o, do, lse, causal=True)  # d = 128
 
 q: [B, Hq, Sq, d], k/v: [B, Hkv, Skv, d], bf16, contiguous, on the GPU;
-d in {64, 128}; Hq a multiple of Hkv (grouped-query attention).
+d in {56, 64, 128} (the backward and the persistent form: d = 128); Hq a
+multiple of Hkv (grouped-query attention).
 """
 
 from __future__ import annotations

@@ -48,20 +48,40 @@ def compile_flags() -> list:
             "-I", INCLUDE, "-I", CSRC]
 
 
-def build(out: str = LIB, verbose: bool = False) -> str:
-    tmp = out + ".tmp"
-    cmd = [hipcc(), *compile_flags(), "-shared", *[os.path.join(CSRC, s) for s in SOURCES],
-           "-o", tmp]
+def _compile(src: str, obj: str, verbose: bool) -> str:
+    cmd = [hipcc(), *compile_flags(), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed building %s" % out)
+        raise RuntimeError("hipcc failed compiling %s" % src)
+    return res.stdout + res.stderr
+
+
+def build(out: str = LIB, verbose: bool = False) -> str:
+    """Compile every source (in parallel, one hipcc per file) and link the library."""
+    import concurrent.futures
+    import tempfile
+
+    with tempfile.TemporaryDirectory(prefix="attn_build_") as tmpd:
+        objs = [os.path.join(tmpd, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+        with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as pool:
+            logs = list(pool.map(lambda so: _compile(os.path.join(CSRC, so[0]), so[1], verbose),
+                                 zip(SOURCES, objs)))
+        tmp = out + ".tmp"
+        cmd = [hipcc(), "--offload-arch=%s" % ARCH, "-fPIC", "-shared", *objs, "-o", tmp]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError("hipcc failed linking %s" % out)
+        logs.append(res.stdout + res.stderr)
     # Surface warnings, except the host pass's note that it does not know the
     # device-only packed-fp32 feature.
     noise = ("packed-fp32-ops' is not a recognized feature",)
-    for line in (res.stdout + res.stderr).splitlines():
+    for line in "".join(logs).splitlines():
         if line.strip() and not any(n in line for n in noise):
             sys.stderr.write(line + "\n")
     os.replace(tmp, out)

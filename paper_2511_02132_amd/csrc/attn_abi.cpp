@@ -48,7 +48,7 @@ int hip_fail(hipError_t e) {
     return ATTN_ERR_HIP;
 }
 
-bool supported_d(int d) { return d == 64 || d == 128; }
+bool supported_d(int d) { return d == 56 || d == 64 || d == 128; }
 
 // Shape checks shared by every entry point.  Offsets inside one head are
 // 32-bit byte offsets, so a head (plus one tile of slack) must stay below 2^31.

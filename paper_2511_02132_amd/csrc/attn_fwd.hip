@@ -58,10 +58,23 @@ namespace {
 
 using namespace dev;
 
-template <int D, bool CAUSAL, int MAPPING, int ORDER>
+// D is the head dimension the kernel computes with (64); DG <= D is the head
+// dimension of the tensors in memory (64, or 56 for DeepSeek-V3-shaped heads,
+// Section 4.5).  Rows of DG elements are read into D-wide LDS and register
+// rows whose last D-DG elements are zero -- the copies of those 16-byte chunks
+// use an out-of-range offset, which the buffer hardware turns into zeros --
+// and only the first DG output columns are stored.  Zero columns change no
+// score and add zero output columns, so the result is that of the DG-wide
+// problem.
+template <int D, int DG, bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs p) {
+    static_assert(DG <= D && DG % 8 == 0, "stored rows are whole 16-byte chunks of the LDS rows");
     constexpr int BM = kBlockM;
     constexpr int BN = kBlockN;
+    constexpr int ROW_BYTES_G = DG * 2;            // a row in memory
+    constexpr int TILE_BYTES_G = BN * ROW_BYTES_G;
+    constexpr int CHUNKS_G = DG / 8;               // 16-byte chunks stored per row
+    constexpr uint32_t kOutOfRange = 0x80000000u;  // past every descriptor: reads zero
     constexpr int KSTEPS = D / 16;             // MFMA k-steps of S^T = K Q^T
     constexpr int DBLK = D / 32;               // 32-row blocks of O^T
     constexpr int CHUNKS_PER_ROW = D / 8;      // 16-byte chunks per K/V row
@@ -91,12 +104,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     }
     const int g = t.hq / (p.Hq / p.Hkv);
 
-    const int64_t q_head = ((int64_t)t.b * p.Hq + t.hq) * p.Sq * D;
-    const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * D;
+    const int64_t q_head = ((int64_t)t.b * p.Hq + t.hq) * p.Sq * DG;
+    const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * DG;
     const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)p.q + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
+        (void *)((const char *)p.q + q_head * 2), 0, p.Sq * ROW_BYTES_G, kBufferFlags);
     const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((char *)p.o + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
+        (void *)((char *)p.o + q_head * 2), 0, p.Sq * ROW_BYTES_G, kBufferFlags);
+    // Byte offset of 16-byte chunk `ch` of row `row` in memory (zeros past DG).
+    auto mem_chunk = [&](const int row, const int ch) -> uint32_t {
+        return ch < CHUNKS_G ? (uint32_t)(row * ROW_BYTES_G + ch * 16) : kOutOfRange;
+    };
 
     // Q^T as the B operand: lane holds Q[row][16kk + 8h .. +7] for each k-step.
     const int q_wave0 = t.m * BM + 32 * w;   // first query row of this wave
@@ -104,8 +121,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     bf16x8 qreg[KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk)
-        qreg[kk] = __builtin_bit_cast(
-            bf16x8, load16(rq, (uint32_t)(my_q * D + 16 * kk + 8 * h) * 2u));
+        qreg[kk] = __builtin_bit_cast(bf16x8, load16(rq, mem_chunk(my_q, 2 * kk + h)));
 
     // K/V tiles go straight from global memory to LDS (buffer_load ... lds):
     // each instruction of a wave fills 1024 contiguous LDS bytes, lane j the
@@ -125,18 +141,18 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         const int slot = (w * IPW + i) * 64 + lane;
         const int row = slot / CHUNKS_PER_ROW;
         const int phys = slot % CHUNKS_PER_ROW;
-        k_src[i] = row * ROW_BYTES + ((phys ^ k_swizzle<D>(row)) * 16);
+        k_src[i] = mem_chunk(row, phys ^ k_swizzle<D>(row));
         const int seg = (phys >> 1) ^ v_swizzle<D>(row);
-        v_src[i] = row * ROW_BYTES + (seg * 2 + (phys & 1)) * 16;
+        v_src[i] = mem_chunk(row, seg * 2 + (phys & 1));
     }
     const char *const k_head = (const char *)p.k + kv_head * 2;
     const char *const v_head = (const char *)p.v + kv_head * 2;
-    const uint32_t kv_bytes = p.Skv * ROW_BYTES;
+    const uint32_t kv_bytes = p.Skv * ROW_BYTES_G;
     const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
     // Copy of tile n of K (or V) into LDS buffer `buf`; the descriptor starts
     // at the tile, so the per-lane offsets stay fixed.
     auto copy_tile = [&](const char *head, const uint32_t *src, const int n, const int buf) __attribute__((always_inline)) {
-        const uint32_t off = (uint32_t)n * TILE_BYTES;
+        const uint32_t off = (uint32_t)n * TILE_BYTES_G;
         const i32x4 d = buffer_words(head + off, kv_bytes - off);
 #pragma unroll
         for (int i = 0; i < IPW; ++i)
@@ -303,37 +319,39 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
             const f32x4 o4 = {oacc[db][4 * j + 0] * inv, oacc[db][4 * j + 1] * inv,
                               oacc[db][4 * j + 2] * inv, oacc[db][4 * j + 3] * inv};
             const bf16x4 ob = __builtin_convertvector(o4, bf16x4);
-            const uint32_t off = (uint32_t)(my_q * D + 32 * db + 8 * j + 4 * h) * 2u;
+            const int col = 32 * db + 8 * j + 4 * h;   // 4 columns, all < DG or all >= DG
+            if (col >= DG) continue;
+            const uint32_t off = (uint32_t)(my_q * DG + col) * 2u;
             __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ob), ro, (int)off, 0, 0);
         }
     }
 }
 
-template <int D, bool CAUSAL, int MAPPING, int ORDER>
+template <int D, int DG, bool CAUSAL, int MAPPING, int ORDER>
 hipError_t launch_order(const KernelArgs &a, int grid, hipStream_t stream) {
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, MAPPING, ORDER>), dim3(grid), dim3(kThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, DG, CAUSAL, MAPPING, ORDER>), dim3(grid), dim3(kThreads),
+                       0, stream, a);
     return hipGetLastError();
 }
 
 // The block-major order inside an XCD's piece exists for mapping 2 only.
-template <int D, bool CAUSAL, int MAPPING>
+template <int D, int DG, bool CAUSAL, int MAPPING>
 hipError_t launch_one(const KernelArgs &a, int grid, hipStream_t stream) {
     switch (MAPPING == ATTN_MAP_SWIZZLED_HEAD_FIRST ? a.order : (a.order & kOrderHeavyFirst)) {
-        case 0: return launch_order<D, CAUSAL, MAPPING, 0>(a, grid, stream);
-        case 1: return launch_order<D, CAUSAL, MAPPING, 1>(a, grid, stream);
-        case 2: return launch_order<D, CAUSAL, MAPPING, (MAPPING == 2 ? 2 : 0)>(a, grid, stream);
-        default: return launch_order<D, CAUSAL, MAPPING, (MAPPING == 2 ? 3 : 1)>(a, grid, stream);
+        case 0: return launch_order<D, DG, CAUSAL, MAPPING, 0>(a, grid, stream);
+        case 1: return launch_order<D, DG, CAUSAL, MAPPING, 1>(a, grid, stream);
+        case 2: return launch_order<D, DG, CAUSAL, MAPPING, (MAPPING == 2 ? 2 : 0)>(a, grid, stream);
+        default: return launch_order<D, DG, CAUSAL, MAPPING, (MAPPING == 2 ? 3 : 1)>(a, grid, stream);
     }
 }
 
-template <int D, bool CAUSAL>
+template <int D, int DG, bool CAUSAL>
 hipError_t launch_mapping(const KernelArgs &a, int mapping, int grid, hipStream_t stream) {
     switch (mapping) {
-        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_one<D, CAUSAL, 0>(a, grid, stream);
-        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_one<D, CAUSAL, 1>(a, grid, stream);
-        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_one<D, CAUSAL, 2>(a, grid, stream);
-        default: return launch_one<D, CAUSAL, 3>(a, grid, stream);
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_one<D, DG, CAUSAL, 0>(a, grid, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_one<D, DG, CAUSAL, 1>(a, grid, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_one<D, DG, CAUSAL, 2>(a, grid, stream);
+        default: return launch_one<D, DG, CAUSAL, 3>(a, grid, stream);
     }
 }
 
@@ -342,8 +360,11 @@ hipError_t launch_mapping(const KernelArgs &a, int mapping, int grid, hipStream_
 hipError_t launch_attn_fwd(const KernelArgs &a, int d, bool causal, int mapping, int grid,
                            hipStream_t stream) {
     if (d == 128) return launch_attn_fwd_d128(a, causal, mapping, grid, stream);
-    return causal ? launch_mapping<64, true>(a, mapping, grid, stream)
-                  : launch_mapping<64, false>(a, mapping, grid, stream);
+    if (d == 56)
+        return causal ? launch_mapping<64, 56, true>(a, mapping, grid, stream)
+                      : launch_mapping<64, 56, false>(a, mapping, grid, stream);
+    return causal ? launch_mapping<64, 64, true>(a, mapping, grid, stream)
+                  : launch_mapping<64, 64, false>(a, mapping, grid, stream);
 }
 
 }  // namespace attn

@@ -5,7 +5,7 @@ Each pass directory holds one rocprofv3 run (``-d DIR -o run -f csv json``) of
     rocprofv3 --pmc <counters> -d DIR -o run -f csv json -- python3 bench.py --profile --workload W
 
 Every (mapping, block order) of the attention kernel is its own kernel symbol
-(``attn_fwd_kernel<d, causal, mapping, order>`` or, for d = 128,
+(``attn_fwd_kernel<d, stored d, causal, mapping, order>`` or, for d = 128,
 ``attn_fwd_pp_kernel<causal, mapping, order>``), so one run per pass
 covers all variants.  The run also holds a one-workgroup launch (it can only
 run on XCD 0) and a 256 MiB device copy, used to attribute counter instances
@@ -30,10 +30,10 @@ from collections import defaultdict
 
 MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
                  "swizzled_block_first"]
-# attn_fwd_kernel<d, causal, mapping, order> (4-wave kernel) and
+# attn_fwd_kernel<d, stored d, causal, mapping, order> (4-wave kernel) and
 # attn_fwd_pp_kernel<causal, mapping, order> (d = 128 two-group kernel); order
 # bit 0 = heavy-first, bit 1 = block-major inside each XCD's piece
-KERNEL_RE = re.compile(r"attn_fwd_(?:kernel<\d+, |pp_kernel<)(true|false), (\d), (\d)>")
+KERNEL_RE = re.compile(r"attn_fwd_(?:kernel<\d+, \d+, |pp_kernel<)(true|false), (\d), (\d)>")
 
 
 def order_suffix(order: int) -> str:

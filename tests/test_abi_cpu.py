@@ -75,7 +75,7 @@ def test_probe_validation():
 
 
 def test_sizes():
-    assert pa.block_m(64) == 128 and pa.block_m(128) == 256
+    assert pa.block_m(64) == 128 and pa.block_m(128) == 256 and pa.block_m(56) == 128
     assert pa.block_n(64) == pa.block_n(128) == 64
     assert pa.lib().attn_block_m(96) == -3
     assert pa.grid_size(1, 32, 8192, 128) == 1024
@@ -101,7 +101,8 @@ def test_stream_roundtrip():
 
 MAP_SHAPES = [(1, 4, 256, 64, 8), (1, 32, 8192, 128, 8), (1, 64, 8192, 128, 8),
               (8, 64, 4096, 128, 8), (1, 16, 131072, 128, 8), (2, 12, 300, 128, 8),
-              (3, 5, 1000, 64, 4), (1, 1, 1, 128, 8), (2, 3, 129, 64, 1), (1, 8, 16384, 128, 8)]
+              (3, 5, 1000, 64, 4), (1, 1, 1, 128, 8), (2, 3, 129, 64, 1), (1, 8, 16384, 128, 8),
+              (1, 128, 8192, 56, 8)]
 
 
 @pytest.mark.parametrize("B,Hq,Sq,d,NX", MAP_SHAPES)

@@ -212,3 +212,62 @@ def test_parity_full_size_sampled_rows(name):
     if causal:
         rep = w["Hq"] // w["Hkv"]
         assert torch.equal(outs[0][:, :, 0, :].cpu(), v[:, :, 0, :].repeat_interleave(rep, dim=1))
+
+
+# ------------------------------------------------------------------ d = 56
+
+
+D56_SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, causal: DeepSeek-V3-shaped heads (Section 4.5), not a
+    # multiple of the matrix-core k-step; zero-padded to 64 inside the kernel
+    (1, 2, 2, 100, 100, True),
+    (2, 8, 2, 257, 300, False),
+    (1, 4, 4, 1000, 1000, True),
+    (1, 3, 3, 1, 1, False),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Sq,Skv,causal", D56_SHAPES)
+def test_parity_d56(B, Hq, Hkv, Sq, Skv, causal):
+    _say("d56 parity", B, Hq, Hkv, Sq, Skv, causal)
+    d = 56
+    q = ai.randn_bf16((B, Hq, Sq, d), 8100 + Sq)
+    k = ai.randn_bf16((B, Hkv, Skv, d), 8101 + Sq)
+    v = ai.randn_bf16((B, Hkv, Skv, d), 8102 + Sq)
+    scale = ai.default_scale(d)
+    qd, kd, vd = _to_dev(q, k, v)
+    outs = [_run(qd, kd, vd, causal, scale, m) for m in ALL_MAPPINGS]
+    ref = oracle.attn_fwd_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), causal, scale)
+    mx, mean = _err(outs[0], ref)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (mx, mean)
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
+    # the padding columns are not written: the tensor stays 56 wide and fully finite
+    assert torch.isfinite(outs[0].float()).all()
+    o2, lse = pa.attn_fwd_lse(qd, kd, vd, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o2, outs[0])
+    rl, _ = oracle.attn_row_stats_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), None,
+                                      oracle.all_rows(B, Hq, Sq), causal, scale)
+    assert np.abs(lse.cpu().numpy().astype(np.float64).ravel() - rl).max() <= 1e-4
+
+
+def test_parity_d56_deepseek_prefill_sampled():
+    """DeepSeek-V3 prefill shape (MHA, 128 heads, d 56, 8K, causal): sampled rows."""
+    B, H, S, d = 1, 128, 8192, 56
+    _say("d56 full size", B, H, S)
+    q = ai.randn_bf16((B, H, S, d), 8200)
+    k = ai.randn_bf16((B, H, S, d), 8201)
+    v = ai.randn_bf16((B, H, S, d), 8202)
+    scale = ai.default_scale(d)
+    qd, kd, vd = _to_dev(q, k, v)
+    o = _run(qd, kd, vd, True, scale, pa.method_variant(True))
+    rng = np.random.default_rng(3)
+    rows = np.stack([np.zeros(48, np.int64), rng.integers(0, H, 48), rng.integers(0, S, 48)], 1)
+    rows[:3, 2] = [0, 8191, 4096]
+    ref = oracle.attn_fwd_rows_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), rows, True,
+                                   scale)
+    got = o.float().cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
+    err = np.abs(got - ref)
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (err.max(), err.mean())
+    assert torch.isfinite(o.float()).all()
