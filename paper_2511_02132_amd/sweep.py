@@ -3,6 +3,8 @@
 * MHA (Section 4.3, Table "mha_sweep"): context 8K/32K/128K x batch 1/2/4/8 x
   heads (Hq = Hkv) 8/16/32/64/128, head dimension 128.
 * GQA (Section 4.4): eight KV heads, Hq = 32/64/128, same contexts and batches.
+* DeepSeek-V3 prefill (Section 4.5): 128 heads of dimension 56
+  (``--family mha --heads 128 --d 56 --contexts 2048 8192 32768 131072``).
 * Backward (Section 4.6, ``--pass bwd``): the gradient kernels of attn_bwd,
   timed after one forward that produced O and the log-sum-exp; the paper's
   study uses 128 heads, 8K/32K/128K and batches 1-2
@@ -61,8 +63,8 @@ def configs(family: str, contexts, batches, heads):
                     yield {"B": B, "Hq": H, "Hkv": GQA_KV_HEADS, "S": S}
 
 
-def flops(c, causal):
-    f = 4.0 * c["B"] * c["Hq"] * c["S"] * c["S"] * D
+def flops(c, causal, d=D):
+    f = 4.0 * c["B"] * c["Hq"] * c["S"] * c["S"] * d
     return f / 2 if causal else f
 
 
@@ -74,6 +76,7 @@ def parse(argv=None):
     p.add_argument("--heads", type=int, nargs="+", default=None,
                    help="query heads (default: the paper's list for the family)")
     p.add_argument("--non-causal", action="store_true")
+    p.add_argument("--d", type=int, default=D, choices=(56, 64, 128), help="head dimension")
     p.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd")
     p.add_argument("--reps", type=int, default=2)
     p.add_argument("--json", default=None, help="append one JSON line per configuration")
@@ -106,13 +109,13 @@ def run(a):
     out = open(a.json, "a") if a.json else None
     for ci, c in enumerate(configs(a.family, a.contexts, a.batches, a.heads)):
         gen.manual_seed(7919 * ci + 1)
-        shape_q = (c["B"], c["Hq"], c["S"], D)
-        shape_kv = (c["B"], c["Hkv"], c["S"], D)
+        shape_q = (c["B"], c["Hq"], c["S"], a.d)
+        shape_kv = (c["B"], c["Hkv"], c["S"], a.d)
         q = torch.randn(shape_q, generator=gen, device=dev, dtype=torch.bfloat16)
         k = torch.randn(shape_kv, generator=gen, device=dev, dtype=torch.bfloat16)
         v = torch.randn(shape_kv, generator=gen, device=dev, dtype=torch.bfloat16)
         o = torch.empty_like(q)
-        scale = 1.0 / D ** 0.5
+        scale = 1.0 / a.d ** 0.5
         times = {n: [] for n, _ in vs}
         reps = 1 if a.profile else a.reps
         if a.which == "bwd":
@@ -143,8 +146,8 @@ def run(a):
                     manifest.append({"config": c, "variant": name})
                 torch.cuda.synchronize()
                 times[name].append(e0.elapsed_time(e1))
-        f = flops(c, causal) * (2.5 if a.which == "bwd" else 1.0)
-        rec = {"family": a.family, "pass": a.which, "causal": causal, **c, "d": D,
+        f = flops(c, causal, a.d) * (2.5 if a.which == "bwd" else 1.0)
+        rec = {"family": a.family, "pass": a.which, "causal": causal, **c, "d": a.d,
                "ms": {n: round(statistics.median(t), 4) for n, t in times.items()},
                "tflops": {n: round(f / statistics.median(t) / 1e9, 1) for n, t in times.items()}}
         line = json.dumps(rec)
@@ -251,9 +254,9 @@ def summarise(a):
         base = "swizzled_head_first" + ("+heavy_first" if causal else "")
     names = [n for n in names if not recs or n in recs[0]["tflops"]]
     which = recs[0].get("pass", "fwd") if recs else "fwd"
-    lines = ["# Mapping sweep: %s %s, d=128, %s" % (
+    lines = ["# Mapping sweep: %s %s, d=%d, %s" % (
         recs[0]["family"].upper() if recs else "?", "backward" if which == "bwd" else "forward",
-        "causal" if causal else "non-causal"), ""]
+        recs[0].get("d", D) if recs else D, "causal" if causal else "non-causal"), ""]
     if which == "bwd":
         lines += ["TFLOP/s of the gradient kernels (D, dK/dV, dQ) in the FlashAttention "
                   "convention: 2.5x the forward's 4*B*Hq*S*S*d (halved when causal).", ""]
