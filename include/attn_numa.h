@@ -50,11 +50,16 @@ enum {
     /* Optional flag for ATTN_MAP_SWIZZLED_HEAD_FIRST only (ATTN_ERR_MAPPING
      * otherwise): each XCD receives exactly the tiles it gets without the
      * flag, but when its contiguous piece of the head-major order is made of
-     * whole heads, it dispatches them block-major across those heads.  MI355X
-     * hands an XCD its workgroups four at a time, one per shader engine, in
-     * order; under a causal mask block-major order makes those four equally
-     * expensive (measured: head-major order left one shader engine with 9%
-     * more work).  Not part of the paper's mappings. */
+     * whole heads, it cuts them into groups of four consecutive heads (the
+     * last group may hold fewer) and dispatches each group block-major.
+     * MI355X hands an XCD its workgroups in order, one per shader engine in
+     * turn (four per XCD); under a causal mask this makes four consecutive
+     * workgroups equally expensive (measured: head-major order left one
+     * shader engine with 9% more work), while the workgroups in flight read
+     * the K/V of only four heads.  Applies only when a head has at most 64
+     * row blocks (the imbalance shrinks like 1/blocks, and at long contexts
+     * head-major order shares K/V better); otherwise the order is unchanged.
+     * Not part of the paper's mappings. */
     ATTN_ORDER_XCD_BLOCK_MAJOR = 0x20
 };
 

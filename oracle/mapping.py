@@ -50,10 +50,17 @@ Order options (not among the paper's mappings):
     starts the expensive blocks first.
   * ``xcd_block_major`` (swizzled head-first only): XCD x's piece of the
     head-major order, when it is made of whole heads (hx of them, starting at
-    L0), is dispatched block-major: its k-th WG takes L = L0 + (k mod hx)*NB +
-    k div hx.  Same tiles per XCD, different order inside the XCD.  The MI355X
-    dispatcher hands an XCD its WGs four at a time, one per shader engine
-    (measured), so under a causal mask this makes those four equally costly.
+    L0), is cut into groups of BLOCK_MAJOR_HEADS = 4 consecutive heads (the
+    last group may hold fewer) and each group is dispatched block-major: the
+    group's row block 0 of each of its heads, then row block 1 of each, and so
+    on.  Same tiles per XCD, different order inside the XCD.  The MI355X
+    dispatcher hands an XCD its WGs one per shader engine in turn, four shader
+    engines per XCD (measured), so under a causal mask four consecutive WGs
+    then cost the same, while the WGs in flight still read the K/V of only
+    four heads.  It applies only when NB <= BLOCK_MAJOR_MAX_BLOCKS = 64: the
+    engine imbalance of head-major order shrinks like 1/NB, and at long
+    contexts the four K/V streams in flight cost more than it saves
+    (measured).
 """
 
 from __future__ import annotations
@@ -64,6 +71,8 @@ NAIVE_BLOCK_FIRST = 0
 NAIVE_HEAD_FIRST = 1
 SWIZZLED_HEAD_FIRST = 2
 SWIZZLED_BLOCK_FIRST = 3
+BLOCK_MAJOR_HEADS = 4
+BLOCK_MAJOR_MAX_BLOCKS = 64
 MAPPINGS = (NAIVE_BLOCK_FIRST, NAIVE_HEAD_FIRST, SWIZZLED_HEAD_FIRST, SWIZZLED_BLOCK_FIRST)
 
 
@@ -120,10 +129,13 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
     elif mapping == SWIZZLED_HEAD_FIRST:
         L = swizzled_rank(wid, N, NX)
         L0, n = xcd_piece(wid % NX, N, NX)
-        if xcd_block_major and L0 % NB == 0 and n % NB == 0:
+        if xcd_block_major and NB <= BLOCK_MAJOR_MAX_BLOCKS and L0 % NB == 0 and n % NB == 0:
             hx = n // NB                       # whole heads in the piece
             k = L - L0                         # position within the XCD's sequence
-            L = L0 + (k % hx) * NB + k // hx   # local head k mod hx, block k div hx
+            first = (k // (BLOCK_MAJOR_HEADS * NB)) * BLOCK_MAJOR_HEADS
+            g = min(BLOCK_MAJOR_HEADS, hx - first)   # heads in k's group
+            j = k - first * NB                 # position within the group
+            L = L0 + (first + j % g) * NB + j // g   # head j mod g, block j div g
         b, hq, m = unravel(L, (B, Hq, NB))
     elif mapping == SWIZZLED_BLOCK_FIRST:
         b, m, j = unravel(wid, (B, NB, Hq))

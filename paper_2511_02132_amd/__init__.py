@@ -28,7 +28,9 @@ SWIZZLED_HEAD_FIRST = 2
 SWIZZLED_BLOCK_FIRST = 3
 # Flag OR-ed into a mapping: dispatch each head's row blocks last-to-first.
 HEAVY_FIRST = 0x10
-# Flag for SWIZZLED_HEAD_FIRST: dispatch each XCD's piece of whole heads block-major.
+# Flag for SWIZZLED_HEAD_FIRST: dispatch each XCD's piece of whole heads block-major
+# within groups of four heads (heads of at most 64 row blocks; longer ones keep
+# head-major order).
 XCD_BLOCK_MAJOR = 0x20
 MAPPINGS = {"naive_block_first": NAIVE_BLOCK_FIRST, "naive_head_first": NAIVE_HEAD_FIRST,
             "swizzled_head_first": SWIZZLED_HEAD_FIRST, "swizzled_block_first": SWIZZLED_BLOCK_FIRST}

@@ -87,6 +87,7 @@ def parse(argv=None):
     p.add_argument("--counters", default=None)
     p.add_argument("--out", default=None)
     p.add_argument("--cmd", default="")
+    p.add_argument("--note", default="", help="extra paragraph for the summary")
     a = p.parse_args(argv)
     if a.heads is None:
         a.heads = list(MHA_HEADS if a.family == "mha" else GQA_QHEADS)
@@ -267,7 +268,9 @@ def summarise(a):
                   "(TCC_HIT + TCC_MISS))."]
     lines += ["", "Variants: NBF naive block-first, NHF naive head-first, SHF swizzled head-first "
               "(the method), SBF swizzled block-first; +hf = heavy-first block order, +bm = "
-              "block-major order inside each XCD's piece.", ""]
+              "block-major order in groups of four heads inside each XCD's piece.", ""]
+    if a.note:
+        lines += [a.note, ""]
     if a.cmd:
         lines += ["Commands:", "", "```", a.cmd, "```", ""]
     hdr = "| S | B | Hq/Hkv | " + " | ".join(sh(n) for n in names) + " |"

@@ -164,7 +164,9 @@ def pin_swizzled_block_first(m):
 def pin_xcd_block_major(m):
     """Order option for swizzled head-first: same XCD tile sets, block-major inside."""
     for (B, Hq, NB, NX) in SHAPES[::3] + [(1, 32, 32, 8), (1, 64, 32, 8), (8, 64, 16, 8),
-                                          (1, 16, 512, 8), (2, 12, 3, 8)]:
+                                          (1, 16, 512, 8), (2, 12, 3, 8), (1, 128, 16, 8),
+                                          (2, 128, 8, 8), (1, 48, 5, 8), (3, 40, 4, 8),
+                                          (1, 16, 64, 8), (1, 16, 65, 8), (1, 32, 128, 8)]:
         N = B * Hq * NB
         for heavy in (False, True):
             plain = _table(m, mp.SWIZZLED_HEAD_FIRST, B, Hq, NB, NX) if not heavy else \
@@ -181,15 +183,26 @@ def pin_xcd_block_major(m):
                 seq = bm[sel]
                 if n == 0:
                     continue
-                if L0 % NB == 0 and n % NB == 0:
+                if NB <= 64 and L0 % NB == 0 and n % NB == 0:
                     hx = n // NB
+                    # the expected order, built by nested loops: groups of four
+                    # local heads in turn, each group block-major
+                    want = []
+                    for g0 in range(0, hx, 4):
+                        group = range(g0, min(g0 + 4, hx))
+                        for blk in range(NB):
+                            for h in group:
+                                want.append((h, blk))
                     blocks = seq[:, 2] if not heavy else NB - 1 - seq[:, 2]
-                    # block-major: block k // hx, heads of the piece in order
-                    assert np.array_equal(blocks, np.arange(n) // hx), (B, Hq, NB, NX, x)
                     heads = seq[:, 0] * Hq + seq[:, 1]
-                    assert np.array_equal(heads - heads.min(), np.arange(n) % hx)
-                    if hx % 4 == 0:   # four consecutive WGs share a row block
-                        assert all(len(set(blocks[i:i + 4])) == 1 for i in range(0, n, 4))
+                    got = list(zip((heads - L0 // NB).tolist(), blocks.tolist()))
+                    assert got == want, (B, Hq, NB, NX, x)
+                    # four consecutive WGs of a full group share a row block
+                    full = (hx // 4) * 4 * NB
+                    assert all(len(set(blocks[i:i + 4])) == 1 for i in range(0, full, 4))
+                    # at most four heads among any 4*NB consecutive WGs of a group
+                    for i in range(0, n, 4 * NB):
+                        assert len(set(heads[i:i + 4 * NB].tolist())) <= 4
                 else:
                     assert np.array_equal(seq, plain[sel])
     with pytest.raises(ValueError):
@@ -283,9 +296,22 @@ class _Mutant:
         self.__dict__.setdefault("bm_rank", _bm_rank)
 
 
-def _bm_rank(L, x, N, NX, NB):
+def _bm_rank(L, x, N, NX, NB, G=4, max_blocks=64):
     L0, n = mp.xcd_piece(x, N, NX)
-    if L0 % NB or n % NB:
+    if NB > max_blocks or L0 % NB or n % NB:
+        return L
+    hx = n // NB
+    k = L - L0
+    first = (k // (G * NB)) * G
+    g = min(G, hx - first)
+    j = k - first * NB
+    return L0 + (first + j % g) * NB + j // g
+
+
+def _bm_rank_whole_piece(L, x, N, NX, NB):
+    """Block-major across all heads of the piece (no groups)."""
+    L0, n = mp.xcd_piece(x, N, NX)
+    if NB > 64 or L0 % NB or n % NB:
         return L
     hx = n // NB
     k = L - L0
@@ -294,18 +320,37 @@ def _bm_rank(L, x, N, NX, NB):
 
 def _bm_rank_transposed(L, x, N, NX, NB):
     L0, n = mp.xcd_piece(x, N, NX)
-    if L0 % NB or n % NB:
+    if NB > 64 or L0 % NB or n % NB:
         return L
     hx = n // NB
     k = L - L0
-    return L0 + (k // hx) * hx + k % hx if hx == NB else L0 + (k // hx) * NB + k % hx
+    first = (k // (4 * NB)) * 4
+    g = min(4, hx - first)
+    j = k - first * NB
+    return L0 + first * NB + (j // NB) + (j % NB) * g if g == NB else L0 + first * NB + j
 
 
 def _bm_rank_any_piece(L, x, N, NX, NB):
     L0, n = mp.xcd_piece(x, N, NX)
+    if NB > 64:
+        return L
     hx = max(1, -(-n // NB))
     k = L - L0
-    return L0 + (k % hx) * NB + k // hx
+    first = (k // (4 * NB)) * 4
+    g = max(1, min(4, hx - first))
+    j = k - first * NB
+    return L0 + (first + j % g) * NB + j // g
+
+
+def _bm_rank_full_last_group(L, x, N, NX, NB):
+    """Treats a short last group as four heads wide."""
+    L0, n = mp.xcd_piece(x, N, NX)
+    if NB > 64 or L0 % NB or n % NB:
+        return L
+    k = L - L0
+    first = (k // (4 * NB)) * 4
+    j = k - first * NB
+    return min(L0 + n - 1, L0 + (first + j % 4) * NB + j // 4)
 
 
 def _unravel_first_fastest(x, radices):
@@ -336,6 +381,12 @@ MAP_MUTANTS = {
     "block_first_swizzle_missing": dict(sbf_head=lambda j, Hq, NX: j),
     "block_major_transposed": dict(bm_rank=_bm_rank_transposed),
     "block_major_on_partial_pieces": dict(bm_rank=_bm_rank_any_piece),
+    "block_major_whole_piece": dict(bm_rank=_bm_rank_whole_piece),
+    "block_major_full_last_group": dict(bm_rank=_bm_rank_full_last_group),
+    "block_major_at_any_length": dict(bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB,
+                                                                             max_blocks=1 << 30)),
+    "block_major_limit_off_by_one": dict(bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB,
+                                                                                max_blocks=63)),
     "block_first_swizzle_transposed": dict(
         sbf_head=lambda j, Hq, NX: (j % (Hq // NX if Hq >= NX else 1)) * NX + j // max(Hq // NX, 1)
         if Hq % NX == 0 else j),
