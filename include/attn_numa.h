@@ -70,7 +70,7 @@ enum {
     ATTN_ERR_UNSUPPORTED = -3, /* head dimension other than 56, 64 or 128 (or a form that lacks it) */
     ATTN_ERR_MAPPING = -4,     /* mapping not one of ATTN_MAP_* */
     ATTN_ERR_SCALE = -5,       /* scale not finite or not > 0 */
-    ATTN_ERR_ALIGN = -6,       /* a tensor pointer not 16-byte aligned */
+    ATTN_ERR_ALIGN = -6,       /* a bf16 tensor not 16-byte aligned, or an fp32/int32 buffer not 4-byte aligned */
     ATTN_ERR_HIP = -7,         /* a HIP runtime call failed; see attn_last_hip_error() */
     ATTN_ERR_ALIAS = -8        /* o overlaps q, k or v */
 };

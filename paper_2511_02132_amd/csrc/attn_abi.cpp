@@ -306,10 +306,10 @@ const char *attn_strerror(int code) {
         case ATTN_OK: return "ok";
         case ATTN_ERR_NULL: return "null pointer argument";
         case ATTN_ERR_SHAPE: return "invalid shape (non-positive dimension, Hq % Hkv != 0, or size limit)";
-        case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (supported: 64, 128)";
+        case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (forward: 56, 64, 128; backward and persistent forward: 128)";
         case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST, and for 2 | ATTN_ORDER_XCD_BLOCK_MAJOR)";
         case ATTN_ERR_SCALE: return "scale must be finite and > 0";
-        case ATTN_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
+        case ATTN_ERR_ALIGN: return "pointer not aligned (bf16 tensors: 16 bytes; fp32 and int32 buffers: 4 bytes)";
         case ATTN_ERR_HIP: return "HIP runtime error";
         case ATTN_ERR_ALIAS: return "output overlaps an input";
         default: return "unknown status code";
