@@ -15,12 +15,17 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libattn_numa.so")
-SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_abi.cpp"]
+SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "attn_abi.cpp"]
+# Per-file options.  attn_bwd_dq.hip keeps its matrix-core accumulators in
+# ordinary vector registers: the compiler's default (accumulators in AGPRs
+# whenever a wave may use more than 256 registers) makes the softmax copy
+# them out and back on every tile.
+FILE_FLAGS = {"attn_bwd_dq.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form"]}
 ARCH = "gfx950"
 
 
-KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_device.h",
-                  "attn_internal.h"]
+KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_bwd_dq.hip",
+                  "attn_bwd_common.h", "attn_device.h", "attn_internal.h"]
 
 
 def kernel_source_hash() -> str:
@@ -41,15 +46,16 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libattn_numa.so)")
 
 
-def compile_flags() -> list:
+def compile_flags(name: str = "") -> list:
+    """hipcc options for source file `name` (its per-file options included)."""
     return ["--offload-arch=%s" % ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
             # packed fp32 VALU ops stay disabled in device code
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-I", INCLUDE, "-I", CSRC]
+            "-I", INCLUDE, "-I", CSRC] + FILE_FLAGS.get(os.path.basename(name), [])
 
 
 def _compile(src: str, obj: str, verbose: bool) -> str:
-    cmd = [hipcc(), *compile_flags(), "-c", src, "-o", obj]
+    cmd = [hipcc(), *compile_flags(src), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -17,7 +17,8 @@
 //      of 32 rows through LDS, keeping the block's K and V rows in registers
 //      and dK, dV in fp32 accumulators, so a GQA group's sum needs no atomics;
 //   3. dQ: one workgroup per (b, query head, block of 128 rows), streaming
-//      K and V tiles of 64 keys like the forward, dQ accumulated in registers.
+//      K and V tiles of 64 keys like the forward, dQ accumulated in registers
+//      (attn_bwd_dq.hip, built with its own register-class option).
 // Splitting dQ from dK/dV recomputes S and dP once more, but every output is
 // written by exactly one workgroup in a fixed order: the gradients are
 // deterministic and bitwise independent of the workgroup mapping.
@@ -46,7 +47,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "attn_device.h"
+#include "attn_bwd_common.h"
 #include "attn_internal.h"
 #include "attn_numa.h"
 
@@ -54,32 +55,7 @@ namespace attn {
 namespace {
 
 using namespace dev;
-
-constexpr int D = 128;
-constexpr int ROW_BYTES = D * 2;
-constexpr int KSTEPS = D / 16;   // MFMA k-steps over the head dimension
-constexpr int DBLK = D / 32;     // 32-row blocks of a transposed gradient
-constexpr float kLog2e = 1.44269504088896340736f;
-
-// Chunk c (16 bytes) of row r of a tile is stored at c ^ dual_swizzle(r).
-//  * 16-byte row reads: 16 consecutive rows, one logical chunk -> the 16
-//    values of dual_swizzle over 16 consecutive rows are all distinct.
-//  * transposing reads: 4 consecutive rows x 64 bytes per 32 lanes -> the
-//    64-byte block index moves by (r & 3) and so differs between the rows.
-__device__ __forceinline__ int dual_swizzle(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
-
-__device__ __forceinline__ uint32_t sw_off(int row, int byte) {
-    return (uint32_t)(row * ROW_BYTES + ((((byte >> 4) ^ dual_swizzle(row)) << 4) | (byte & 15)));
-}
-
-// Global source offset (within a tile) of LDS slot `slot` (16 bytes) of a
-// dual-swizzled tile: the copies fill LDS linearly and fetch the chunk that
-// belongs there.
-__device__ __forceinline__ uint32_t slot_src(int slot) {
-    const int row = slot / 16;
-    const int phys = slot % 16;
-    return (uint32_t)(row * ROW_BYTES + ((phys ^ dual_swizzle(row)) << 4));
-}
+using namespace bwd;
 
 // ---------------------------------------------------------------- D = <dO, O>
 
@@ -100,53 +76,6 @@ __global__ __launch_bounds__(256) void attn_bwd_delta_kernel(const BwdArgs p) {
     acc += __shfl_xor(acc, 2, 16);
     acc += __shfl_xor(acc, 1, 16);
     if (row < rows && part == 0) p.delta[row] = acc;
-}
-
-// Per-lane offsets of the transposing read of a dual-swizzled tile: lane i of
-// 16-lane group gsel addresses row 4h + i/4 of a 16-row chunk (+8 rows for the
-// upper half of the operand) and columns 32db + 16gsel + 4(i%4).  The chunk's
-// first row (16kc + 8hi) is a multiple of 4, so the swizzle of the addressed
-// row depends only on (i/4, h, hi) and the chunk offset is an immediate.
-__device__ __forceinline__ void tr_offsets(int lane, uint32_t (&off)[DBLK][2]) {
-    const int li = lane & 15;
-    const int gsel = (lane >> 4) & 1;
-    const int h = lane >> 5;
-#pragma unroll
-    for (int db = 0; db < DBLK; ++db)
-#pragma unroll
-        for (int hi = 0; hi < 2; ++hi) {
-            const int row = 8 * hi + 4 * h + (li >> 2);   // row within a 16-row chunk
-            const int byte = 64 * db + 32 * gsel + 8 * (li & 3);
-            off[db][hi] = sw_off(row, byte) - 8 * hi * ROW_BYTES;
-        }
-}
-
-// A operand rows 16kc.. of a transposing read (see tr_offsets).
-__device__ __forceinline__ bf16x8 tr_operand(lds_char *base, const uint32_t (&off)[DBLK][2], int db,
-                                             int kc) {
-    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (lds_bf16x4 *)(base + off[db][0] + 16 * kc * ROW_BYTES));
-    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (lds_bf16x4 *)(base + off[db][1] + (16 * kc + 8) * ROW_BYTES));
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// Rows of a transposed accumulator (lane holds column c; register r of block
-// db holds row 32db + 8(r/4) + 4h + r%4) scaled and stored as bf16 rows:
-// `row` of the output head, bounded by the descriptor.
-__device__ __forceinline__ void store_rows(const f32x16 (&acc)[DBLK], float s,
-                                           __amdgpu_buffer_rsrc_t r, int row, int h) {
-#pragma unroll
-    for (int db = 0; db < DBLK; ++db) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const f32x4 v4 = {acc[db][4 * j + 0] * s, acc[db][4 * j + 1] * s,
-                              acc[db][4 * j + 2] * s, acc[db][4 * j + 3] * s};
-            const bf16x4 b4 = __builtin_convertvector(v4, bf16x4);
-            const uint32_t off = (uint32_t)(row * D + 32 * db + 8 * j + 4 * h) * 2u;
-            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, b4), r, (int)off, 0, 0);
-        }
-    }
 }
 
 // ---------------------------------------------------------------- dK, dV
@@ -310,162 +239,15 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(const BwdArgs p) 
     store_rows(dvacc, 1.0f, rdv, my_key, h);
 }
 
-// ---------------------------------------------------------------- dQ
-
-constexpr int kRowsPerWg = 128;
-constexpr int kKeyTile = 64;
-
-template <bool CAUSAL, int MAPPING, int ORDER>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(const BwdArgs p) {
-    constexpr int BN = kKeyTile;
-    constexpr int TILE = BN * ROW_BYTES;   // 16 KiB: K or V rows of one tile
-    constexpr int STAGE = 2 * TILE;
-    constexpr int IPW = TILE / 1024 / 4;   // copy instructions per wave per tile
-    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
-    lds_char *const lds = (lds_char *)smem;
-    const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int c = lane & 31;
-    const int h = lane >> 5;
-
-    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NBQ, p.NX);
-    const int g = t.hq / (p.Hq / p.Hkv);
-    const int q_wave0 = t.m * kRowsPerWg + 32 * w;
-    const int my_q = q_wave0 + c;
-
-    const int64_t q_head = ((int64_t)t.b * p.Hq + t.hq) * p.Sq;   // row index of the head's row 0
-    const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * D;
-    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)p.q + q_head * ROW_BYTES), 0, p.Sq * ROW_BYTES, kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rdo = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)p.dout + q_head * ROW_BYTES), 0, p.Sq * ROW_BYTES, kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rstat = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(p.lse + q_head), 0, p.Sq * 4, kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rdelta = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(p.delta + q_head), 0, p.Sq * 4, kBufferFlags);
-    // Q and dO rows as B operands (lane: row my_q, columns 16kk + 8h .. +7);
-    // rows past Sq read zeros, and so do their statistics.
-    bf16x8 qreg[KSTEPS], doreg[KSTEPS];
-#pragma unroll
-    for (int kk = 0; kk < KSTEPS; ++kk) {
-        const uint32_t off = (uint32_t)(my_q * D + 16 * kk + 8 * h) * 2u;
-        qreg[kk] = __builtin_bit_cast(bf16x8, load16(rq, off));
-        doreg[kk] = __builtin_bit_cast(bf16x8, load16(rdo, off));
-    }
-    const float lse2 = __builtin_bit_cast(
-        float, __builtin_amdgcn_raw_buffer_load_b32(rstat, my_q * 4, 0, 0)) * kLog2e;
-    const float dq_d = __builtin_bit_cast(
-        float, __builtin_amdgcn_raw_buffer_load_b32(rdelta, my_q * 4, 0, 0));
-
-    const int kv_end = CAUSAL ? min((t.m + 1) * kRowsPerWg, p.Skv) : p.Skv;
-    const int n_tiles = (kv_end + BN - 1) / BN;
-    const uint32_t kv_bytes = p.Skv * ROW_BYTES;
-    const uint32_t kv_lim = min(kv_bytes, (uint32_t)n_tiles * TILE);
-    uint32_t src[IPW];
-#pragma unroll
-    for (int i = 0; i < IPW; ++i) src[i] = slot_src((w * IPW + i) * 64 + lane);
-    const char *const k_head = (const char *)p.k + kv_head * 2;
-    const char *const v_head = (const char *)p.v + kv_head * 2;
-    auto copy_tile = [&](const int n, const int buf) __attribute__((always_inline)) {
-        const uint32_t off = (uint32_t)n * TILE;
-        const uint32_t left = off < kv_lim ? kv_lim - off : 0u;
-        const i32x4 dk_ = buffer_words(k_head + (off < kv_lim ? off : 0u), left);
-        const i32x4 dv_ = buffer_words(v_head + (off < kv_lim ? off : 0u), left);
-        const uint32_t dst = lds_base + buf * STAGE;
-#pragma unroll
-        for (int i = 0; i < IPW; ++i) {
-            lds_copy16(dk_, src[i], dst + (w * IPW + i) * 1024);
-            lds_copy16(dv_, src[i], dst + TILE + (w * IPW + i) * 1024);
-        }
-    };
-
-    uint32_t row_off[KSTEPS];   // A operand rows: row c (+32 kb2), logical chunk 2kk + h
-#pragma unroll
-    for (int kk = 0; kk < KSTEPS; ++kk) row_off[kk] = sw_off(c, (2 * kk + h) * 16);
-    uint32_t tro[DBLK][2];
-    tr_offsets(lane, tro);
-
-    f32x16 dqacc[DBLK];
-#pragma unroll
-    for (int db = 0; db < DBLK; ++db)
-        for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.0f;
-    const float sl2 = p.scale_log2;
-
-    auto compute = [&](const int n, auto buf_c) __attribute__((always_inline)) {
-        constexpr int BUF = decltype(buf_c)::value;
-        lds_char *const kb = lds + BUF * STAGE;
-        lds_char *const vb = kb + TILE;
-        f32x16 sacc[2] = {}, dpacc[2] = {};
-#pragma unroll
-        for (int kk = 0; kk < KSTEPS; ++kk) {
-#pragma unroll
-            for (int kb2 = 0; kb2 < 2; ++kb2) {
-                const bf16x8 ak = *(const lds_bf16x8 *)(kb + row_off[kk] + kb2 * 32 * ROW_BYTES);
-                sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, qreg[kk], sacc[kb2], 0, 0, 0);
-                const bf16x8 av = *(const lds_bf16x8 *)(vb + row_off[kk] + kb2 * 32 * ROW_BYTES);
-                dpacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, doreg[kk], dpacc[kb2], 0, 0, 0);
-            }
-        }
-        // Register r of block kb2 holds key 32kb2 + 8(r/4) + 4h + r%4 of the tile.
-        const int key0 = n * BN;
-        const bool need_mask = CAUSAL && key0 + BN - 1 > q_wave0;
-        f32x8 ds8[4];
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float pr = exp2_hw(__builtin_fmaf(sacc[kb2][r], sl2, -lse2));
-                const int key = key0 + 32 * kb2 + 8 * (r >> 2) + 4 * h + (r & 3);
-                if (need_mask && key > my_q) pr = 0.0f;
-                ds8[2 * kb2 + (r >> 3)][r & 7] = pr * (dpacc[kb2][r] - dq_d);
-            }
-        bf16x8 dsb[4];
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) dsb[kc] = __builtin_convertvector(ds8[kc], bf16x8);
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc)
-#pragma unroll
-            for (int db = 0; db < DBLK; ++db)
-                dqacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(kb, tro, db, kc),
-                                                                     dsb[kc], dqacc[db], 0, 0, 0);
-    };
-
-    copy_tile(0, 0);
-    for (int n = 0; n < n_tiles; n += 2) {
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-        __syncthreads();
-        if (n + 1 < n_tiles) copy_tile(n + 1, 1);
-        compute(n, Int<0>{});
-        if (n + 1 < n_tiles) {
-            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-            __syncthreads();
-            if (n + 2 < n_tiles) copy_tile(n + 2, 0);
-            compute(n + 1, Int<1>{});
-        }
-    }
-
-    const __amdgpu_buffer_rsrc_t rdq = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((char *)p.dq + q_head * ROW_BYTES), 0, p.Sq * ROW_BYTES, kBufferFlags);
-    store_rows(dqacc, p.scale, rdq, my_q, h);
-}
-
 // ---------------------------------------------------------------- launchers
 
 template <bool CAUSAL, int MAPPING, int ORDER>
 hipError_t launch_grads(const BwdArgs &a, hipStream_t stream) {
     const int g_kv = a.B * a.Hkv * a.NKV;
-    const int g_q = a.B * a.Hq * a.NBQ;
     // The dK/dV kernel's natural order already starts with the heaviest causal
     // key block; it takes only the block-major bit.
     hipLaunchKernelGGL((attn_bwd_dkdv_kernel<CAUSAL, MAPPING, (ORDER & kOrderXcdBlockMajor)>),
                        dim3(g_kv), dim3(256), 0, stream, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<CAUSAL, MAPPING, ORDER>), dim3(g_q), dim3(256), 0,
-                       stream, a);
     return hipGetLastError();
 }
 
@@ -498,8 +280,10 @@ hipError_t launch_attn_bwd(const BwdArgs &a, bool causal, int mapping, hipStream
                        stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return causal ? launch_grads_mapping<true>(a, mapping, stream)
-                  : launch_grads_mapping<false>(a, mapping, stream);
+    e = causal ? launch_grads_mapping<true>(a, mapping, stream)
+               : launch_grads_mapping<false>(a, mapping, stream);
+    if (e != hipSuccess) return e;
+    return launch_attn_bwd_dq(a, causal, mapping, stream);
 }
 
 }  // namespace attn

@@ -160,5 +160,7 @@ hipError_t launch_attn_fwd_d128(const KernelArgs &args, bool causal, int mapping
                                 hipStream_t stream);
 // The backward pass (attn_bwd.hip): D, then dK/dV, then dQ, on one stream.
 hipError_t launch_attn_bwd(const BwdArgs &args, bool causal, int mapping, hipStream_t stream);
+// The dQ kernel alone (attn_bwd_dq.hip); launch_attn_bwd calls it last.
+hipError_t launch_attn_bwd_dq(const BwdArgs &args, bool causal, int mapping, hipStream_t stream);
 
 }  // namespace attn

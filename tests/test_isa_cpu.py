@@ -27,7 +27,7 @@ import pytest
 
 from paper_2511_02132_amd import build as B
 
-KERNEL_FILES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip"]
+KERNEL_FILES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_bwd_dq.hip"]
 
 # Instructions that read M0 implicitly on gfx9-family targets.
 IMPLICIT_M0 = re.compile(
@@ -55,8 +55,8 @@ pytestmark = pytest.mark.skipif(not _have_hipcc(), reason="hipcc not installed")
 def listings(tmp_path_factory):
     out = {}
     d = tmp_path_factory.mktemp("isa")
-    flags = [f for f in B.compile_flags() if f not in ("-fPIC", "-Wall")]
     for name in KERNEL_FILES:
+        flags = [f for f in B.compile_flags(name) if f not in ("-fPIC", "-Wall")]
         dst = os.path.join(d, name + ".s")
         cmd = [B.hipcc(), *flags, "--cuda-device-only", "-S", os.path.join(B.CSRC, name),
                "-o", dst]
@@ -157,3 +157,8 @@ def test_no_scratch_no_spills_and_resources_fit(listings, name):
         waves_per_simd = max(1, threads // 256)
         assert regs * waves_per_simd <= 512, (md["name"], regs, threads)
         assert lds <= 160 * 1024, (md["name"], lds)
+        if "attn_bwd_dq_kernel" in md["name"]:
+            # built for two workgroups per CU: both fit in registers and LDS,
+            # and the accumulators stay out of AGPRs
+            assert regs <= 256 and int(md.get("agpr_count", "0")) == 0, (md["name"], regs)
+            assert 2 * lds <= 160 * 1024, (md["name"], lds)
