@@ -83,8 +83,12 @@ __global__ __launch_bounds__(256) void attn_bwd_delta_kernel(const BwdArgs p) {
 constexpr int kKeysPerWg = 128;
 constexpr int kQTile = 32;
 
+// Declared for two waves per SIMD (two workgroups per CU): the compiler then
+// keeps it within 256 registers by spilling three of the K/V operand registers
+// (48 bytes per lane, reloaded once per query tile), and the second workgroup
+// more than hides the reloads.
 template <bool CAUSAL, int MAPPING, int ORDER>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(const BwdArgs p) {
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) {
     constexpr int BQ = kQTile;
     constexpr int TILE = BQ * ROW_BYTES;          // 8 KiB: Q or dO rows of one tile
     constexpr int STAT = 1024;                     // 32 fp32 row statistics (one 64-lane copy)
