@@ -114,8 +114,5 @@ struct Int {
     static constexpr int value = V;
 };
 
-// Lazy rescaling threshold (exp2 domain): probabilities stay below 2^8.
-constexpr float kLazy = 8.0f;
-
 }  // namespace dev
 }  // namespace attn

@@ -204,9 +204,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     for (int db = 0; db < DBLK; ++db)
         for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
     // Online-softmax state of this lane's query row.  m_ref is the reference
-    // maximum the exponents are taken against; it is raised (and O, l rescaled)
-    // only when a score exceeds it by more than 2^kLazy in the exp2 domain, so
-    // every probability stays <= 2^kLazy.  Any reference gives the same result
+    // maximum the exponents are taken against: set from the first tile's row
+    // maximum and raised (O and l rescaled) only when a tile's exponentials
+    // sum to more than 2^24 for some lane.  Any reference gives the same result
     // in exact arithmetic, because O and l are divided by the same factor.
     float m_ref = -__builtin_inff();
     float mb = -__builtin_inff();   // m_ref * scale_log2
@@ -244,14 +244,32 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
                     s_cur[kb2][r] = dead ? -__builtin_inff() : s_cur[kb2][r];
                 }
         }
-        // Maximum over this lane's scores of the tile (tile 0 holds key 0, so
-        // every row has a finite score there).
-        float mx = s_cur[0][0];
+        // Exponentials against the current reference and their sum over this
+        // lane's keys.  The sum shows, without a maximum over the tile, whether
+        // the reference is unset (first tile: inf/NaN) or a score exceeds it by
+        // more than 2^24 in the exp2 domain; only then is the row maximum
+        // taken, O and l rescaled and the exponentials recomputed.
+        f32x8 p8[4];
+        auto exps = [&]() __attribute__((always_inline)) {
+            float ts = 0.0f;
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
+            for (int kc = 0; kc < 4; ++kc)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kb2][r]);
-        if (__any((mx - m_ref) * sl2 > kLazy)) {
+                for (int e = 0; e < 8; ++e)
+                    p8[kc][e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
+#pragma unroll
+            for (int kc = 0; kc < 4; ++kc)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ts += p8[kc][e];
+            return ts;
+        };
+        float tsum = exps();
+        if (__any(!(tsum <= 16777216.0f))) {
+            float mx = s_cur[0][0];
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kb2][r]);
             // Raise the reference to the row maximum (both lane halves agree).
             const float m_new = fmaxf(m_ref, fmaxf(mx, xor32(mx)));
             const float alpha = exp2_hw((m_ref - m_new) * sl2);   // 0 on the first tile
@@ -262,7 +280,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
                 for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
             m_ref = m_new;
             mb = m_ref * sl2;
+            tsum = exps();
         }
+        l_run += tsum;
 
         // Scores of the next tile, independent of the work below so the two
         // interleave.  After the last tile this reads a stale (in-bounds)
@@ -277,14 +297,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         for (int kb2 = 0; kb2 < 2; ++kb2) {
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                f32x8 p8;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float pr = exp2_hw(__builtin_fmaf(s_cur[kb2][8 * u + e], sl2, -mb));
-                    p8[e] = pr;
-                    l_run += pr;
-                }
-                const bf16x8 pb = __builtin_convertvector(p8, bf16x8);
+                const bf16x8 pb = __builtin_convertvector(p8[2 * kb2 + u], bf16x8);
                 const int chunk = (16 * (2 * kb2 + u)) * ROW_BYTES;
 #pragma unroll
                 for (int db = 0; db < DBLK; ++db) {
