@@ -1,0 +1,142 @@
+"""CPU tests of the measurement tooling: the kernel-name decoding and counter
+arithmetic behind profiles/ (rocprof_counters), the mapping-sweep summary
+(sweep), and bench.py's host-side checks.  No GPU is used."""
+
+import json
+import math
+import os
+import subprocess
+import sys
+from types import SimpleNamespace
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402  (imports torch only inside main())
+import paper_2511_02132_amd as pa  # noqa: E402
+from paper_2511_02132_amd import rocprof_counters as rc  # noqa: E402
+from paper_2511_02132_amd import sweep  # noqa: E402
+
+
+def _order_bits(mapping):
+    return (1 if mapping & pa.HEAVY_FIRST else 0) | (2 if mapping & pa.XCD_BLOCK_MAJOR else 0)
+
+
+def test_variant_of_kernel_names():
+    ns = "void attn::(anonymous namespace)::"
+    cases = {
+        ns + "attn_fwd_pp_kernel<true, 2, 3>(attn::KernelArgs)":
+            "swizzled_head_first+heavy_first+xcd_block_major",
+        ns + "attn_fwd_pp_kernel<false, 0, 0>(attn::KernelArgs)": "naive_block_first",
+        ns + "attn_fwd_kernel<64, 56, true, 3, 1>(attn::KernelArgs)":
+            "swizzled_block_first+heavy_first",
+        ns + "attn_fwd_kernel<64, 64, false, 1, 0>(attn::KernelArgs)": "naive_head_first",
+        # not forward launches of the dispatched kernels
+        ns + "attn_fwd_pp_persistent_kernel<true, 2, 3>(attn::KernelArgs)": None,
+        ns + "attn_bwd_dq_kernel<true, 2, 3>(attn::BwdArgs)": None,
+        "__amd_rocclr_copyBuffer": None,
+    }
+    for name, want in cases.items():
+        assert rc.variant_of(name) == want, name
+    # every variant the measurements compare decodes from its kernel name
+    for causal in (False, True):
+        for vname, m in pa.variants(causal):
+            kname = ns + "attn_fwd_pp_kernel<%s, %d, %d>(attn::KernelArgs)" % (
+                "true" if causal else "false", m & 0xF, _order_bits(m))
+            assert rc.variant_of(kname) == vname
+
+
+def _write_counters(d, rows):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_counter_collection.csv"), "w") as f:
+        f.write("Dispatch_Id,Kernel_Name,Grid_Size,Counter_Name,Counter_Value\n")
+        for did, kname, grid, cname, val in rows:
+            f.write('%d,"%s",%d,%s,%r\n' % (did, kname, grid, cname, val))
+
+
+def test_counter_summary_arithmetic(tmp_path):
+    """Hit rate, copy-kernel scale factors and HBM bytes from known counter values."""
+    k_swz = "void attn::(anonymous namespace)::attn_fwd_pp_kernel<true, 2, 1>(attn::KernelArgs)"
+    k_nbf = "void attn::(anonymous namespace)::attn_fwd_pp_kernel<true, 0, 1>(attn::KernelArgs)"
+    copy = "__amd_rocclr_copyBuffer"
+    mib256_kib = 256 * 1024
+    a = str(tmp_path / "A")
+    b = str(tmp_path / "B")
+    _write_counters(a, [
+        (1, copy, 1 << 20, "TCC_HIT", 5.0),
+        (2, k_swz, 512 * 1024, "TCC_HIT", 900.0), (2, k_swz, 512 * 1024, "TCC_MISS", 100.0),
+        (3, k_swz, 512 * 1024, "TCC_HIT", 700.0), (3, k_swz, 512 * 1024, "TCC_MISS", 300.0),
+        (4, k_nbf, 512 * 1024, "TCC_HIT", 250.0), (4, k_nbf, 512 * 1024, "TCC_MISS", 750.0),
+        # a one-workgroup launch (grid <= 512) is the XCD check, not a measurement
+        (5, k_swz, 512, "TCC_HIT", 1.0), (5, k_swz, 512, "TCC_MISS", 1e6),
+    ])
+    _write_counters(b, [
+        # the copy kernel's FETCH_SIZE reads half of the 256 MiB it moved
+        (1, copy, 1 << 20, "FETCH_SIZE", mib256_kib / 2), (1, copy, 1 << 20, "WRITE_SIZE", mib256_kib),
+        (2, k_swz, 512 * 1024, "FETCH_SIZE", 1000.0), (2, k_swz, 512 * 1024, "WRITE_SIZE", 500.0),
+        (3, k_swz, 512 * 1024, "FETCH_SIZE", 3000.0), (3, k_swz, 512 * 1024, "WRITE_SIZE", 500.0),
+    ])
+    result, fetch_fac, write_fac, xcc0 = rc.summarise([a, b], "mha_b1_h32_s8192_d128_causal")
+    assert fetch_fac == pytest.approx(2.0) and write_fac == pytest.approx(1.0)
+    assert xcc0 is None   # no per-XCC records in these directories
+    swz = result["swizzled_head_first+heavy_first"]
+    assert swz["l2_hit_rate"] == pytest.approx(0.8)   # (900+700) / 2000
+    assert swz["hbm_bytes_per_launch"] == int(2000 * 1024 * 2.0 + 500 * 1024 * 1.0)
+    assert result["naive_block_first+heavy_first"]["l2_hit_rate"] == pytest.approx(0.25)
+    assert "hbm_bytes_per_launch" not in result["naive_block_first+heavy_first"]
+
+
+def test_compulsory_bytes():
+    # MHA B1 H32 S8192 d128: Q, K, V, O once each, bf16
+    assert rc.compulsory_bytes("mha_b1_h32_s8192_d128_causal") == 4 * 32 * 8192 * 128 * 2
+    # GQA: K and V have 8 heads
+    assert rc.compulsory_bytes("gqa_b1_hq64_hkv8_s8192_d128_causal") == \
+        (2 * 64 + 2 * 8) * 8192 * 128 * 2
+
+
+def test_sweep_summary(tmp_path):
+    names = [n for n, _ in pa.variants(True)]
+    recs = []
+    for i, (S, B) in enumerate([(8192, 1), (32768, 2)]):
+        tf = {n: 500.0 + 10 * j + 100 * i for j, n in enumerate(names)}
+        recs.append({"family": "mha", "pass": "fwd", "causal": True, "S": S, "B": B, "Hq": 32,
+                     "Hkv": 32, "d": 128, "ms": {n: 1.0 for n in names}, "tflops": tf})
+    timing = tmp_path / "t.jsonl"
+    timing.write_text("".join(json.dumps(r) + "\n" for r in recs))
+    out = tmp_path / "s.md"
+    args = SimpleNamespace(timing=[str(timing)], counters=None, manifest=None, out=str(out),
+                           cmd="CMD", note="NOTE")
+    sweep.summarise(args)
+    text = out.read_text()
+    assert text.startswith("# Mapping sweep: MHA forward, d=128, causal")
+    assert "NOTE" in text and "CMD" in text
+    rows = [l for l in text.splitlines() if l.startswith("| 8K") or l.startswith("| 32K")]
+    assert len(rows) == 2 and all(l.count("|") == 3 + len(names) + 1 for l in rows)
+    base = pa.variant_name(pa.method_variant(True))
+    for n in names:
+        g = math.exp(sum(math.log(r["tflops"][n] / r["tflops"][base]) for r in recs) / 2)
+        assert "- %s: %.3f" % (n, g) in text
+
+
+def test_bench_refuses_several_gpus():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_bench_uses_counters_of_this_kernel_source_only(tmp_path, monkeypatch):
+    wl = "mha_b1_h32_s8192_d128_causal"
+    os.makedirs(tmp_path / "profiles")
+    path = tmp_path / "profiles" / ("attn_fwd_%s_counters.md" % wl)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.counter_summary(wl) is None   # no summary at all
+    for sha, found in ((bench.kernel_source_hash(), True), ("0" * 16, False)):
+        data = {"kernel_source_sha256": sha, "per_mapping": {"x": {"hbm_bytes_per_launch": 7}}}
+        path.write_text("# counters\n\n```json\n%s\n```\n" % json.dumps(data))
+        got = bench.counter_summary(wl)
+        assert (got is not None) == found
+        if found:
+            assert got["per_mapping"]["x"]["hbm_bytes_per_launch"] == 7
