@@ -179,7 +179,7 @@ def write_md(out: str, workload: str, cmd: str, result, fetch_fac, write_fac, xc
     lines = ["# attn_fwd counters: %s" % workload, "",
              "rocprofv3 counter passes over `bench.py --profile` (2 launches per variant; "
              "values are per launch, averaged).", "",
-             "Commands (from the repository root on the GPU box; `cd /tmp` first, "
+             "Commands (run from the repository root; `cd /tmp` first, "
              "paths absolute in the run):", "", "```", cmd.strip(), "```", "",
              "Compulsory HBM bytes (Q, K, V read once, O written once): %d (%.1f MiB)."
              % (comp, comp / 2 ** 20), ""]
@@ -218,7 +218,7 @@ def write_stats_md(out: str, stats_csv: str, bench_json: str, cmd: str):
     bench = json.loads(line)
     head = bench["config"]["mapping"]
     lines = ["# attn_fwd kernel trace: %s" % bench["config"]["workload"], "",
-             "Command (repository root on the GPU box; `cd /tmp` first, paths absolute):", "",
+             "Command (run from the repository root; `cd /tmp` first, paths absolute):", "",
              "```", cmd.strip(), "```", "",
              "Kernel source sha256[:16]: `%s`" % kernel_source_hash(), "",
              "| kernel | calls | average us | min us | max us | share |",
