@@ -451,10 +451,20 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
     if (grp == 0) barrier_lds();
 
     // O = acc / l, rounded to bf16; lane holds d = 32db + 8j + 4h + 0..3 of its row.
+    // The wave's 32 rows are consecutive in O, so they leave through LDS as
+    // whole rows: each store instruction then writes 1 KiB of consecutive
+    // bytes instead of 32 separate 16-byte pieces.  After the last barrier no
+    // wave reads the stage buffers and every copy into them has landed, so
+    // wave w can use bytes [8 KiB w, 8 KiB (w+1)) of them; no other wave
+    // touches that range before the next tile's prologue (a persistent
+    // workgroup passes a barrier first).  Chunks are swizzled as in a K tile, so
+    // the 16 chunks of a row that one read instruction takes hit distinct banks.
     const float l_tot = lsum + xor32(lsum);
     const float inv = 1.0f / l_tot;
     store_lse(p.lse == nullptr ? nullptr : p.lse + ((int64_t)t.b * p.Hq + t.hq) * p.Sq, p.Sq, my_q,
               lane, mb, l_tot);
+    static_assert(WAVES * 32 * ROW_BYTES <= kStages * STAGE_BYTES, "O staging exceeds the stage buffers");
+    lds_char *const ow = lds + w * 32 * ROW_BYTES;
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
 #pragma unroll
@@ -462,9 +472,20 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
             const f32x4 o4 = {oacc[db][4 * jj + 0] * inv, oacc[db][4 * jj + 1] * inv,
                               oacc[db][4 * jj + 2] * inv, oacc[db][4 * jj + 3] * inv};
             const bf16x4 ob = __builtin_convertvector(o4, bf16x4);
-            const uint32_t off = (uint32_t)(my_q * D + 32 * db + 8 * jj + 4 * h) * 2u;
-            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ob), ro, (int)off, 0, 0);
+            const int q = 4 * db + jj;
+            *(lds_u32x2 *)(ow + c * ROW_BYTES + ((q ^ k_swizzle<D>(c)) * 16) + 8 * h) =
+                __builtin_bit_cast(u32x2, ob);
         }
+    }
+    // One wave's LDS accesses complete in order; this only keeps the compiler
+    // from hoisting the reads above the writes of other lanes.
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int r = 4 * i + (lane >> 4);
+        const int q = lane & 15;
+        const u32x4 val = *(const lds_u32x4 *)(ow + r * ROW_BYTES + ((q ^ k_swizzle<D>(r)) * 16));
+        __builtin_amdgcn_raw_buffer_store_b128(val, ro, (q_wave0 + r) * ROW_BYTES + q * 16, 0, 0);
     }
 }
 
