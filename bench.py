@@ -16,6 +16,11 @@ the same) -- inputs already resident in HBM.  Prints ONE JSON line:
               WRITE_SIZE (scaled by a copy kernel of known size), read from
               the committed counter summary when it was taken on this kernel
               source, else null
+  mfma_ceiling  the dense bf16 MFMA rate this chip sustains, measured live by
+              a kernel of register-operand MFMAs only (attn_calib_mfma), with
+              the shader clock it runs at; frac = value / that rate.  The
+              published peak assumes the 2.4 GHz peak clock, which a sustained
+              matrix-core load does not get
   per_mapping TFLOP/s of all four mappings (for causal workloads also each
               with the heavy-first block order) and of swizzled head-first with
               block-major order inside each XCD, interleaved, cold (L2 and MALL
@@ -23,6 +28,11 @@ the same) -- inputs already resident in HBM.  Prints ONE JSON line:
               L2 hit rate from the counter summary
   cpu_baseline  the fp64 CPU oracle on a time-bounded sample of the same
               workload's rows, in TFLOP/s of the same flop count
+
+The default warm-up (60 steps, about 30 ms of work at the default workload)
+outlasts the power manager's response to the start of a matrix-core load: the
+shader clock dips for some tens of milliseconds before it settles, and the K
+timed steps measure the settled rate.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
        python bench.py --profile [--workload NAME]   (kernel launches only, for rocprofv3)
@@ -73,8 +83,8 @@ def counter_summary(workload: str):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=60)
     p.add_argument("--workload", default=DEFAULT_WORKLOAD)
     p.add_argument("--reps", type=int, default=10, help="cold reps per mapping")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -152,6 +162,16 @@ def main():
     print("headline: %.4f ms/step, %.1f TFLOP/s (wall %.3f s)" % (ms_per_step, value, wall),
           file=sys.stderr, flush=True)
 
+    # ---- compute ceiling: dense bf16 MFMA on register operands, after the
+    # headline so that the clock has settled; the later half of the launches
+    calib = pa.calib_mfma(dev, launches=8, stream=stream)
+    settled = calib[len(calib) // 2:]
+    ceiling = {"tflops": round(statistics.median(c["tflops"] for c in settled), 1),
+               "clock_mhz": round(statistics.median(c["clock_mhz"] for c in settled)),
+               "launches": len(settled)}
+    ceiling["frac"] = round(value / ceiling["tflops"], 4)
+    print("mfma ceiling: %s" % json.dumps(ceiling), file=sys.stderr, flush=True)
+
     # ---- per mapping: interleaved, cold (L2 + MALL flushed) and warm, median
     flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device=dev)
     vs = variants(causal)
@@ -208,6 +228,7 @@ def main():
                    "block_m": pa.block_m(d), "block_n": pa.block_n(d), "num_xcd": pa.num_xcd(),
                    "flop_convention": "4*B*Hq*Sq*Skv*d, halved when causal"},
         "roofline": roofline,
+        "mfma_ceiling": ceiling,
         "per_mapping": per_mapping,
         "cpu_baseline": cpu,
         "kernel_source_sha256": kernel_source_hash(),

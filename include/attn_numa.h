@@ -224,6 +224,27 @@ int attn_block_n(int d);
  * current device (cached per device).  Negative ATTN_ERR_* on failure. */
 int attn_num_xcd(void);
 
+/*
+ * attn_calib_mfma -- calibration of the compute ceiling that the roofline is
+ * read against; not part of the paper's method.  The published dense bf16
+ * peak assumes the peak engine clock, which a sustained matrix-core load does
+ * not get.  Launches `grid` workgroups of 512 threads whose 8 waves each
+ * issue 4*iters independent dense bf16 MFMAs (32x32x16, 32768 flop each) on
+ * register operands, with no memory or LDS traffic: 32768*4*iters*8*grid flop
+ * in total.  Asynchronous on the calling thread's stream.
+ * rec  : device pointer to 4*grid int64, owned by the caller; workgroup g
+ *        writes rec[4g+0], rec[4g+1] = the 100 MHz real-time counter at its
+ *        start and end, and rec[4g+2], rec[4g+3] = the shader-clock counter at
+ *        its start and end, so that (rec[4g+3]-rec[4g+2]) /
+ *        (rec[4g+1]-rec[4g+0]) * 100 MHz is the clock it ran at.
+ * sink : device pointer to 512*grid float, owned by the caller; receives
+ *        values that only keep the products live.
+ * grid in [1, 65536] and iters a positive multiple of 4 up to 2^24
+ * (ATTN_ERR_SHAPE); rec 8-byte and sink 4-byte aligned (ATTN_ERR_ALIGN); the
+ * two must not overlap (ATTN_ERR_ALIAS).
+ */
+int attn_calib_mfma(int grid, int iters, int64_t *rec, float *sink);
+
 /* Stream for subsequent calls from the calling thread (a hipStream_t; NULL is
  * the null stream).  The library does not take ownership. */
 int attn_set_stream(void *hip_stream);

@@ -83,6 +83,7 @@ SIGNATURES = {
     "attn_fwd_lse": ([_vp, _vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_fwd_persistent": ([_vp] * 7 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_bwd": ([_vp] * 10 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
+    "attn_calib_mfma": ([_ci, _ci, _vp, _vp], _ci),
     "attn_grid_size": ([_ci, _ci, _ci, _ci], ctypes.c_int64),
     "attn_map_tiles": ([_ci, _ci, _ci, _ci, _ci, _ci, _i32p], _ci),
     "attn_block_m": ([_ci], _ci),
@@ -308,6 +309,43 @@ def attn_bwd(q, k, v, o, dout, lse, dq=None, dk=None, dv=None, delta=None, *,
                           int(bool(causal)), scale, int(mapping)),
            "attn_bwd")
     return dq, dk, dv
+
+
+CALIB_THREADS = 512
+
+
+def calib_mfma(device=None, *, grid: int | None = None, iters: int = 20000, launches: int = 8,
+               stream=None) -> list:
+    """Matrix-core calibration (attn_calib_mfma), `launches` launches back to back.
+
+    Per launch: its time from HIP events on the stream (ms), the dense bf16
+    rate (TFLOP/s) and the median shader clock of its workgroups (MHz).  The
+    grid defaults to one workgroup per compute unit."""
+    import torch
+    device = torch.device(device if device is not None else "cuda")
+    torch.cuda.set_device(device)
+    if grid is None:
+        grid = torch.cuda.get_device_properties(device).multi_processor_count
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    lib().attn_set_stream(ctypes.c_void_p(stream.cuda_stream))
+    rec = torch.zeros((launches, grid, 4), dtype=torch.int64, device=device)
+    sink = torch.empty(grid * CALIB_THREADS, dtype=torch.float32, device=device)
+    flop = 32768.0 * 4 * iters * 8 * grid
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    events[0].record(stream)
+    for i in range(launches):
+        _check(lib().attn_calib_mfma(grid, iters, rec[i].data_ptr(), sink.data_ptr()),
+               "attn_calib_mfma")
+        events[i + 1].record(stream)
+    torch.cuda.synchronize(device)
+    r = rec.cpu().numpy().astype(np.float64)
+    out = []
+    for i in range(launches):
+        ms = events[i].elapsed_time(events[i + 1])
+        mhz = (r[i, :, 3] - r[i, :, 2]) / (r[i, :, 1] - r[i, :, 0]) * 100.0
+        out.append({"ms": ms, "tflops": flop / ms / 1e9, "clock_mhz": float(np.median(mhz))})
+    return out
 
 
 def attention_flops(B: int, Hq: int, Sq: int, Skv: int, d: int, causal: bool) -> float:

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libattn_numa.so")
-SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "attn_abi.cpp"]
+SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "attn_calib.hip",
+           "attn_abi.cpp"]
 # Per-file options.  attn_bwd_dq.hip keeps its matrix-core accumulators in
 # ordinary vector registers: the compiler's default (accumulators in AGPRs
 # whenever a wave may use more than 256 registers) makes the softmax copy

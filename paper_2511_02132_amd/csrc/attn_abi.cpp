@@ -11,6 +11,7 @@
 #include <cstdlib>
 #include <cstring>
 
+#include "attn_calib.h"
 #include "attn_internal.h"
 #include "attn_numa.h"
 
@@ -249,6 +250,18 @@ int attn_fwd_probe(const void *q, const void *k, const void *v, void *o, int B, 
     return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe, nullptr);
 }
 
+int attn_calib_mfma(int grid, int iters, int64_t *rec, float *sink) {
+    if (!rec || !sink) return ATTN_ERR_NULL;
+    if (grid <= 0 || grid > attn::kCalibMaxGrid || iters <= 0 || iters % 4 != 0 ||
+        iters > attn::kCalibMaxIters)
+        return ATTN_ERR_SHAPE;
+    if (((uintptr_t)rec & 7u) || ((uintptr_t)sink & 3u)) return ATTN_ERR_ALIGN;
+    if (overlaps(rec, (int64_t)grid * 4 * 8, sink, (int64_t)grid * attn::kCalibThreads * 4))
+        return ATTN_ERR_ALIAS;
+    const hipError_t e = attn::launch_calib_mfma(grid, iters, rec, sink, t_stream);
+    return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
 int64_t attn_grid_size(int B, int Hq, int Sq, int d) {
     if (B <= 0 || Hq <= 0 || Sq <= 0 || d <= 0) return ATTN_ERR_SHAPE;
     if (!supported_d(d)) return ATTN_ERR_UNSUPPORTED;
@@ -309,7 +322,7 @@ const char *attn_strerror(int code) {
         case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (forward: 56, 64, 128; backward and persistent forward: 128)";
         case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST, and for 2 | ATTN_ORDER_XCD_BLOCK_MAJOR)";
         case ATTN_ERR_SCALE: return "scale must be finite and > 0";
-        case ATTN_ERR_ALIGN: return "pointer not aligned (bf16 tensors: 16 bytes; fp32 and int32 buffers: 4 bytes)";
+        case ATTN_ERR_ALIGN: return "pointer not aligned (bf16 tensors: 16 bytes; fp32 and int32 buffers: 4 bytes; int64 buffers: 8 bytes)";
         case ATTN_ERR_HIP: return "HIP runtime error";
         case ATTN_ERR_ALIAS: return "output overlaps an input";
         default: return "unknown status code";

@@ -122,3 +122,18 @@ def test_map_tiles_errors():
     ptr = out.ctypes.data_as(pa._i32p)
     assert pa.lib().attn_map_tiles(5, 1, 4, 256, 64, 8, ptr) == -4
     assert pa.lib().attn_map_tiles(2, 1, 4, 256, 64, 0, ptr) == -2
+
+
+def test_calib_validation():
+    lib = pa.lib()
+    R, S = 0x50000000, 0x60000000
+    assert lib.attn_calib_mfma(256, 20000, None, S) == -1
+    assert lib.attn_calib_mfma(256, 20000, R, None) == -1
+    assert lib.attn_calib_mfma(0, 20000, R, S) == -2
+    assert lib.attn_calib_mfma(65537, 4, R, S) == -2
+    assert lib.attn_calib_mfma(256, 0, R, S) == -2
+    assert lib.attn_calib_mfma(256, 6, R, S) == -2          # not a multiple of 4
+    assert lib.attn_calib_mfma(256, 2 ** 24 + 4, R, S) == -2
+    assert lib.attn_calib_mfma(256, 4, R + 4, S) == -6      # int64 records: 8-byte aligned
+    assert lib.attn_calib_mfma(256, 4, R, S + 2) == -6
+    assert lib.attn_calib_mfma(256, 4, R, R + 8) == -8      # sink overlaps the records
