@@ -103,6 +103,7 @@ def main():
               "shard heads across GPUs with no exchange). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    import numpy as np
     import torch
 
     import attn_inputs as ai
@@ -170,6 +171,10 @@ def main():
                "clock_mhz": round(statistics.median(c["clock_mhz"] for c in settled)),
                "launches": len(settled)}
     ceiling["frac"] = round(value / ceiling["tflops"], 4)
+    # dense bf16 peak at that clock: CUs x 4 SIMDs x 1024 flop per cycle
+    n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
+    ceiling["peak_at_clock_tflops"] = round(n_cu * 4 * 1024 * ceiling["clock_mhz"] * 1e6 / 1e12, 1)
+    ceiling["frac_of_peak_at_clock"] = round(value / ceiling["peak_at_clock_tflops"], 4)
     print("mfma ceiling: %s" % json.dumps(ceiling), file=sys.stderr, flush=True)
 
     # ---- per mapping: interleaved, cold (L2 + MALL flushed) and warm, median
@@ -196,7 +201,8 @@ def main():
         cm, wm = statistics.median(cold[name]), statistics.median(warm[name])
         ent = {"cold_ms": round(cm, 5), "cold_tflops": round(flops / cm / 1e9, 2),
                "warm_ms": round(wm, 5), "warm_tflops": round(flops / wm / 1e9, 2),
-               "cold_ms_min": round(min(cold[name]), 5), "cold_ms_max": round(max(cold[name]), 5)}
+               "cold_ms_min": round(min(cold[name]), 5), "cold_ms_max": round(max(cold[name]), 5),
+               "cold_ms_iqr": round(float(np.subtract(*np.percentile(cold[name], [75, 25]))), 5)}
         if counters:
             c = counters["per_mapping"].get(name, {})
             ent["l2_hit_rate"] = c.get("l2_hit_rate")
@@ -236,6 +242,18 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (first processor in /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(args, w, q, k, v, scale):
     """Time the oracle on random rows of the workload for about args.cpu_seconds."""
     import numpy as np
@@ -258,7 +276,7 @@ def cpu_baseline(args, w, q, k, v, scale):
         nrows += chunk
         chunk = min(chunk * 2, 4096)
     return {"value": round(total_flop / total_s / 1e12, 6), "unit": "TFLOP/s",
-            "cores": oracle.max_threads(), "kind": "oracle",
+            "cores": oracle.max_threads(), "cpu_model": cpu_model(), "kind": "oracle",
             "sample": "%d uniformly drawn (b, hq, row) query rows of %s, %.1f GFLOP (4*|keys|*d "
                       "per row) in %.1f s, fp64 two-pass softmax" % (
                           nrows, args.workload, total_flop / 1e9, total_s)}

@@ -140,3 +140,9 @@ def test_bench_uses_counters_of_this_kernel_source_only(tmp_path, monkeypatch):
         assert (got is not None) == found
         if found:
             assert got["per_mapping"]["x"]["hbm_bytes_per_launch"] == 7
+
+
+def test_bench_cpu_model_is_named():
+    import bench
+    name = bench.cpu_model()
+    assert isinstance(name, str) and name
