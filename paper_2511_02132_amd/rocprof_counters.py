@@ -93,6 +93,20 @@ def per_xcc(d: str, counters=("TCC_HIT", "TCC_MISS")):
     return out
 
 
+def read_hit_bounds(hit: float, read: float, write: float):
+    """Bounds on the L2 hit rate of read requests alone.
+
+    The counters give hits and misses of all requests (TCC_HIT, TCC_MISS) and
+    the number of read and write requests (TCC_READ, TCC_WRITE), but not how
+    the hits split between reads and writes.  Every hit is a read hit when no
+    write hits (upper bound), and at most TCC_WRITE hits are write hits (lower
+    bound).  The all-request rate depends on how stores are split into
+    requests; this one measures the reuse of what the kernel reads."""
+    if read <= 0:
+        return None
+    return [round(max(0.0, hit - write) / read, 4), round(min(1.0, hit / read), 4)]
+
+
 def summarise(dirs, workload: str):
     per_variant = defaultdict(lambda: defaultdict(list))
     copy = defaultdict(list)
@@ -144,7 +158,13 @@ def summarise(dirs, workload: str):
                                for x in range(8)])
             if xs:
                 ent["l2_hit_rate_per_xcd"] = [round(sum(col) / len(col), 4) for col in zip(*xs)]
-        for c in ("TCC_HIT", "TCC_MISS", "TCC_EA0_RDREQ", "TCC_EA0_RDREQ_32B",
+            if vals.get("TCC_READ") and "TCC_WRITE" in vals:
+                ent["l2_read_hit_rate_bounds"] = read_hit_bounds(
+                    vals["TCC_HIT"], vals["TCC_READ"], vals["TCC_WRITE"])
+                ent["l2_requests_read_write_over_hit_miss"] = round(
+                    (vals["TCC_READ"] + vals["TCC_WRITE"]) /
+                    max(1.0, vals["TCC_HIT"] + vals["TCC_MISS"]), 4)
+        for c in ("TCC_HIT", "TCC_MISS", "TCC_READ", "TCC_WRITE", "TCC_EA0_RDREQ", "TCC_EA0_RDREQ_32B",
                   "TCC_EA0_RDREQ_DRAM", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS",
                   "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VALU",
                   "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"):
@@ -189,14 +209,18 @@ def write_md(out: str, workload: str, cmd: str, result, fetch_fac, write_fac, xc
     if xcc0_share is not None:
         lines.append("XCD attribution check: %.4f of the one-workgroup launch's L2 requests "
                      "land on XCD 0 instances." % xcc0_share)
-    lines += ["", "| variant | L2 hit | L2 hit per XCD (min..max) | HBM bytes / launch | "
+    lines += ["L2 read hit: bounds on the hit rate of read requests alone, from TCC_HIT, "
+              "TCC_READ and TCC_WRITE (between no write hitting and every write hitting).", ""]
+    lines += ["", "| variant | L2 hit | L2 read hit | L2 hit per XCD (min..max) | HBM bytes / launch | "
                   "/ compulsory | MFMA util % | LDS bank-conflict cycles |",
-              "|---|---|---|---|---|---|---|"]
+              "|---|---|---|---|---|---|---|---|"]
     for v, e in result.items():
         px = e.get("l2_hit_rate_per_xcd")
         hb = e.get("hbm_bytes_per_launch")
-        lines.append("| %s | %s | %s | %s | %s | %s | %s |" % (
+        rb = e.get("l2_read_hit_rate_bounds")
+        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s |" % (
             v, "%.1f%%" % (100 * e["l2_hit_rate"]) if "l2_hit_rate" in e else "-",
+            "%.1f..%.1f%%" % (100 * rb[0], 100 * rb[1]) if rb else "-",
             "%.1f..%.1f%%" % (100 * min(px), 100 * max(px)) if px else "-",
             "%.3e" % hb if hb else "-", "%.2f" % (hb / comp) if hb else "-",
             e.get("mfma_util_pct", "-"), "%.3e" % e["sq_lds_bank_conflict"]

@@ -179,8 +179,28 @@ def _variant_of(kernel_name: str):
 BWD_RE = re.compile(r"attn_bwd_(dkdv|dq)_kernel<(true|false), (\d), (\d)>")
 
 
+L2_COUNTERS = ("TCC_HIT", "TCC_MISS", "TCC_READ", "TCC_WRITE")
+
+
 def l2_by_launch(counters_dir: str, manifest_path: str):
-    """{(B, Hq, Hkv, S, variant): l2 hit rate} from a --profile run under rocprofv3 --pmc.
+    """{(B, Hq, Hkv, S, variant): l2 hit rate} from a --profile run under rocprofv3 --pmc."""
+    return {k: v["TCC_HIT"] / max(v["TCC_HIT"] + v["TCC_MISS"], 1.0)
+            for k, v in l2_counters_by_launch(counters_dir, manifest_path).items()}
+
+
+def l2_read_bounds_by_launch(counters_dir: str, manifest_path: str):
+    """{(B, Hq, Hkv, S, variant): [low, high]} bounds on the L2 hit rate of read
+    requests alone, where the run also counted TCC_READ and TCC_WRITE."""
+    from paper_2511_02132_amd.rocprof_counters import read_hit_bounds
+    out = {}
+    for k, v in l2_counters_by_launch(counters_dir, manifest_path).items():
+        if v.get("TCC_READ"):
+            out[k] = read_hit_bounds(v["TCC_HIT"], v["TCC_READ"], v.get("TCC_WRITE", 0.0))
+    return out
+
+
+def l2_counters_by_launch(counters_dir: str, manifest_path: str):
+    """{(B, Hq, Hkv, S, variant): {counter: value}} of the L2 counters of each launch.
 
     For the backward, one manifest entry is one attn_bwd call: its dK/dV and
     dQ dispatches are summed (the D kernel is the same for every mapping)."""
@@ -212,8 +232,9 @@ def l2_by_launch(counters_dir: str, manifest_path: str):
                 merged.append(dict(rec))
             else:
                 prev = merged[-1]
-                for key in ("TCC_HIT", "TCC_MISS"):
-                    prev[key] = prev.get(key, 0.0) + rec.get(key, 0.0)
+                for key in L2_COUNTERS:
+                    if key in rec:
+                        prev[key] = prev.get(key, 0.0) + rec[key]
                 prev["variant"] = rec["variant"]   # the dQ kernel carries every order bit
         launches = merged
     if len(launches) != len(manifest):
@@ -224,8 +245,10 @@ def l2_by_launch(counters_dir: str, manifest_path: str):
         if rec["variant"] != m["variant"]:
             raise ValueError("launch order differs from the manifest")
         c = m["config"]
-        hit, miss = rec.get("TCC_HIT", 0.0), rec.get("TCC_MISS", 0.0)
-        out[(c["B"], c["Hq"], c["Hkv"], c["S"], m["variant"])] = hit / max(hit + miss, 1.0)
+        vals = {key: rec[key] for key in L2_COUNTERS if key in rec}
+        vals.setdefault("TCC_HIT", 0.0)
+        vals.setdefault("TCC_MISS", 0.0)
+        out[(c["B"], c["Hq"], c["Hkv"], c["S"], m["variant"])] = vals
     return out
 
 
@@ -239,6 +262,7 @@ def summarise(a):
                     recs[(r["S"], r["B"], r["Hq"], r["Hkv"])] = r
     recs = [recs[k] for k in sorted(recs)]
     l2 = l2_by_launch(a.counters, a.manifest) if a.counters else {}
+    l2r = l2_read_bounds_by_launch(a.counters, a.manifest) if a.counters else {}
     causal = recs[0]["causal"] if recs else True
     names = [n for n, _ in variants(causal)]
     short = {"naive_block_first": "NBF", "naive_head_first": "NHF", "swizzled_head_first": "SHF",
@@ -266,6 +290,9 @@ def summarise(a):
     if l2:
         lines += ["Second table: L2 hit rate of one launch per variant (rocprofv3 TCC_HIT / "
                   "(TCC_HIT + TCC_MISS))."]
+    if l2r:
+        lines += ["Third table: bounds on the L2 hit rate of read requests alone (TCC_HIT, "
+                  "TCC_READ, TCC_WRITE: between no write hitting and every write hitting)."]
     lines += ["", "Variants: NBF naive block-first, NHF naive head-first, SHF swizzled head-first "
               "(the method), SBF swizzled block-first; +hf = heavy-first block order, +bm = "
               "block-major order in groups of four heads inside each XCD's piece.", ""]
@@ -287,6 +314,15 @@ def summarise(a):
             for n in names:
                 h = l2.get((r["B"], r["Hq"], r["Hkv"], r["S"], n))
                 cells.append("-" if h is None else "%.1f%%" % (100 * h))
+            lines.append("| %dK | %d | %d/%d | %s |" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"],
+                                                       " | ".join(cells)))
+    if l2r:
+        lines += ["", hdr, "|" + "---|" * (3 + len(names))]
+        for r in recs:
+            cells = []
+            for n in names:
+                b = l2r.get((r["B"], r["Hq"], r["Hkv"], r["S"], n))
+                cells.append("-" if b is None else "%.1f..%.1f%%" % (100 * b[0], 100 * b[1]))
             lines.append("| %dK | %d | %d/%d | %s |" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"],
                                                        " | ".join(cells)))
     # geometric-mean speed relative to the method, per variant

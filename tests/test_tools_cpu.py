@@ -146,3 +146,29 @@ def test_bench_cpu_model_is_named():
     import bench
     name = bench.cpu_model()
     assert isinstance(name, str) and name
+
+
+def test_read_hit_bounds():
+    # 1000 requests: 900 reads, 100 writes, 800 hits.  If no write hits, all 800
+    # hits are reads (800/900); if all 100 writes hit, 700 are (700/900).
+    lo, hi = rc.read_hit_bounds(800.0, 900.0, 100.0)
+    assert lo == pytest.approx(700 / 900, abs=1e-4) and hi == pytest.approx(800 / 900, abs=1e-4)
+    # more writes than hits: the lower bound stops at zero; no reads: no bound
+    assert rc.read_hit_bounds(50.0, 900.0, 100.0)[0] == 0.0
+    assert rc.read_hit_bounds(50.0, 0.0, 100.0) is None
+
+
+def test_counter_summary_read_hit_bounds(tmp_path):
+    k_swz = "void attn::(anonymous namespace)::attn_fwd_pp_kernel<true, 2, 1>(attn::KernelArgs)"
+    a = str(tmp_path / "A")
+    e = str(tmp_path / "E")
+    _write_counters(a, [(2, k_swz, 512 * 1024, "TCC_HIT", 800.0),
+                        (2, k_swz, 512 * 1024, "TCC_MISS", 200.0)])
+    _write_counters(e, [(2, k_swz, 512 * 1024, "TCC_READ", 900.0),
+                        (2, k_swz, 512 * 1024, "TCC_WRITE", 100.0)])
+    result, _, _, _ = rc.summarise([a, e], "mha_b1_h32_s8192_d128_causal")
+    swz = result["swizzled_head_first+heavy_first"]
+    assert swz["l2_hit_rate"] == pytest.approx(0.8)
+    assert swz["l2_read_hit_rate_bounds"] == [pytest.approx(0.7778, abs=1e-4),
+                                              pytest.approx(0.8889, abs=1e-4)]
+    assert swz["l2_requests_read_write_over_hit_miss"] == pytest.approx(1.0)
