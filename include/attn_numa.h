@@ -125,7 +125,10 @@ int attn_fwd_probe(const void *q, const void *k, const void *v, void *o,
  * attn_fwd_lse -- attn_fwd that also writes each row's log-sum-exp, the
  * statistic the backward pass recomputes P from (Section 2.3.1):
  *   lse[b][hq][i] = log sum_{j in J_i} exp(scale * <Q[b,hq,i], K[b,g,j]>)
- * (natural log, fp32; J_i as in attn_fwd).
+ * (natural log, fp32; J_i as in attn_fwd).  For d = 128 the sum is an fp32
+ * sum of the fp32 exponentials.  For d = 56 and 64 it is taken over the
+ * exponentials rounded to bf16 (the weights the output product uses), so lse
+ * is within ln(1 + 2^-8) < 3.9e-3 of the exact value plus fp32 rounding.
  * lse : device pointer to B*Hq*Sq fp32, 4-byte aligned, owned by the caller;
  *     must not overlap q, k, v or o.  Other arguments and behaviour as
  *     attn_fwd.
@@ -173,7 +176,8 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
 /*
  * attn_fwd_persistent -- attn_fwd (optionally also writing lse, as
  * attn_fwd_lse) in a persistent, dispatch-independent form (head dimension 128
- * only): one workgroup per compute unit reads the XCD it runs on (XCC_ID) and
+ * only): one workgroup per compute unit (or per tile, if there are fewer tiles)
+ * reads the XCD it runs on (XCC_ID) and
  * takes tiles from a queue per XCD.  Queue x hands out the workgroup ids
  * wid = x + NX*t, t = 0, 1, ..., i.e. exactly the tiles the round-robin
  * dispatcher of Section 2.2 would send to XCD x under `mapping`, in the same

@@ -145,11 +145,13 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.order = order_bits(mapping);
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
     int grid = B * Hq * a.NB;
-    if (queue) {   // persistent form: one workgroup per compute unit
+    if (queue) {   // persistent form: one workgroup per compute unit, or per tile if fewer
         const int ncu = num_cu();
         if (ncu < 0) return ncu;
         if (nx > attn::kQueueMaxXcd) return ATTN_ERR_UNSUPPORTED;
-        grid = ncu;
+        // With more workgroups than tiles the idle ones would take other XCDs'
+        // tiles before those XCDs' own workgroups start.
+        grid = grid < ncu ? grid : ncu;
     }
     hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, mapping & 0xf, grid, t_stream);
     if (e != hipSuccess) return hip_fail(e);

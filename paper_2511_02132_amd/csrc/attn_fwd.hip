@@ -58,6 +58,14 @@ namespace {
 
 using namespace dev;
 
+// a + b + acc for two bf16 values, in fp32 (one v_dot2 against (1, 1)).
+__device__ __forceinline__ float sum_bf16_pair(__bf16 a, __bf16 b, float acc) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t v = {a, b};
+    const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(v, ones, acc, false);
+}
+
 // D is the head dimension the kernel computes with (64); DG <= D is the head
 // dimension of the tensors in memory (64, or 56 for DeepSeek-V3-shaped heads,
 // Section 4.5).  Rows of DG elements are read into D-wide LDS and register
@@ -249,19 +257,26 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         // the reference is unset (first tile: inf/NaN) or a score exceeds it by
         // more than 2^24 in the exp2 domain; only then is the row maximum
         // taken, O and l rescaled and the exponentials recomputed.
-        f32x8 p8[4];
+        // P is rounded to bf16 (the output product's B operand) as it is formed,
+        // and the row sum is taken from the bf16 pairs, one v_dot2 against
+        // (1, 1) per pair: half the vector instructions of fp32 adds, in a
+        // kernel whose vector ALU, not its matrix core, sets the pace.  The
+        // sum is then that of exactly the weights the output product uses.
+        bf16x8 pb8[4];
         auto exps = [&]() __attribute__((always_inline)) {
-            float ts = 0.0f;
+            float ts[2] = {0.0f, 0.0f};
 #pragma unroll
-            for (int kc = 0; kc < 4; ++kc)
+            for (int kc = 0; kc < 4; ++kc) {
+                f32x8 p8;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    p8[kc][e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
+                    p8[e] = exp2_hw(__builtin_fmaf(s_cur[kc >> 1][8 * (kc & 1) + e], sl2, -mb));
+                pb8[kc] = __builtin_convertvector(p8, bf16x8);
 #pragma unroll
-            for (int kc = 0; kc < 4; ++kc)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) ts += p8[kc][e];
-            return ts;
+                for (int e = 0; e < 4; ++e)
+                    ts[kc & 1] = sum_bf16_pair(pb8[kc][2 * e], pb8[kc][2 * e + 1], ts[kc & 1]);
+            }
+            return ts[0] + ts[1];
         };
         float tsum = exps();
         if (__any(!(tsum <= 16777216.0f))) {
@@ -297,7 +312,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
         for (int kb2 = 0; kb2 < 2; ++kb2) {
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                const bf16x8 pb = __builtin_convertvector(p8[2 * kb2 + u], bf16x8);
+                const bf16x8 pb = pb8[2 * kb2 + u];
                 const int chunk = (16 * (2 * kb2 + u)) * ROW_BYTES;
 #pragma unroll
                 for (int db = 0; db < DBLK; ++db) {

@@ -249,7 +249,7 @@ def test_parity_d56(B, Hq, Hkv, Sq, Skv, causal):
     assert torch.equal(o2, outs[0])
     rl, _ = oracle.attn_row_stats_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), None,
                                       oracle.all_rows(B, Hq, Sq), causal, scale)
-    assert np.abs(lse.cpu().numpy().astype(np.float64).ravel() - rl).max() <= 1e-4
+    assert np.abs(lse.cpu().numpy().astype(np.float64).ravel() - rl).max() <= lse_tolerance(56)
 
 
 def test_parity_d56_deepseek_prefill_sampled():
@@ -284,11 +284,24 @@ LSE_SHAPES = [
 ]
 
 
+def lse_tolerance(d: int) -> float:
+    """Bound on |lse_gpu - lse_oracle| (natural log).
+
+    d = 128: the row sum is the fp32 sum of the fp32 exponentials; 1e-4 covers
+    the fp32 rounding of scores, exponentials, sum and logarithm.
+    d = 56, 64: the row sum is taken over the exponentials rounded to bf16 (the
+    weights the output product uses).  Rounding to nearest with 8 significant
+    bits changes each positive term by at most 2^-8 of itself, so the sum by
+    at most 2^-8 of itself and its logarithm by at most ln(1 + 2^-8) < 3.9e-3;
+    with the fp32 part, 4e-3."""
+    return 1e-4 if d == 128 else 4e-3
+
+
 @pytest.mark.parametrize("B,Hq,Hkv,Sq,Skv,d,causal", LSE_SHAPES)
 def test_forward_lse_all_head_dims(B, Hq, Hkv, Sq, Skv, d, causal):
     """attn_fwd_lse: the row log-sum-exp (natural log of the scaled, masked scores)
-    matches the oracle within 1e-4 for every head dimension, and O is bitwise
-    the plain forward's."""
+    matches the oracle within lse_tolerance(d) for every head dimension, and O is
+    bitwise the plain forward's."""
     _say("lse", B, Hq, Hkv, Sq, Skv, d, causal)
     q = ai.randn_bf16((B, Hq, Sq, d), 9100 + d)
     k = ai.randn_bf16((B, Hkv, Skv, d), 9101 + d)
@@ -303,5 +316,5 @@ def test_forward_lse_all_head_dims(B, Hq, Hkv, Sq, Skv, d, causal):
                                            oracle.all_rows(B, Hq, Sq), causal, scale)
         got = lse.cpu().numpy().astype(np.float64).ravel()
         assert np.isfinite(got).all()
-        assert np.abs(got - ref).max() <= 1e-4, (m, np.abs(got - ref).max())
+        assert np.abs(got - ref).max() <= lse_tolerance(d), (m, np.abs(got - ref).max())
         assert torch.equal(o, _run(qd, kd, vd, causal, scale, m))

@@ -64,9 +64,13 @@ def test_persistent_equals_dispatched(B, Hq, Hkv, Sq, Skv, causal):
         want = mp.enumerate_mapping(mapping, B, Hq, Sq, pa.block_m(128), nx, heavy_first=heavy,
                                     xcd_block_major=xbm)
         assert np.array_equal(rec[:, :3], want), hex(value)
-        on_own_xcd = np.mean(rec[:, 3] == np.arange(n) % nx)
-        # tiles leave their XCD only when taken from another queue at the end
-        assert on_own_xcd >= (0.5 if n < 1024 else 0.9), (hex(value), on_own_xcd)
+        # Tiles leave their XCD only when taken from another queue at the end.
+        # Checked where every XCD's queue holds several tiles: on a grid of a
+        # few tiles, whichever workgroup asks first may take one, which changes
+        # neither the result nor the speed.
+        if n >= 8 * nx:
+            on_own_xcd = np.mean(rec[:, 3] == np.arange(n) % nx)
+            assert on_own_xcd >= (0.5 if n < 1024 else 0.9), (hex(value), on_own_xcd)
 
 
 def test_persistent_reuses_queue_back_to_back():
