@@ -50,17 +50,20 @@ Order options (not among the paper's mappings):
     starts the expensive blocks first.
   * ``xcd_block_major`` (swizzled head-first only): XCD x's piece of the
     head-major order, when it is made of whole heads (hx of them, starting at
-    L0), is cut into groups of BLOCK_MAJOR_HEADS = 4 consecutive heads (the
-    last group may hold fewer) and each group is dispatched block-major: the
+    L0), is cut into groups of G consecutive heads (the last group may hold
+    fewer) and each group is dispatched block-major: the
     group's row block 0 of each of its heads, then row block 1 of each, and so
     on.  Same tiles per XCD, different order inside the XCD.  The MI355X
     dispatcher hands an XCD its WGs one per shader engine in turn, four shader
     engines per XCD (measured), so under a causal mask four consecutive WGs
     then cost the same, while the WGs in flight still read the K/V of only
-    four heads.  It applies only when NB <= BLOCK_MAJOR_MAX_BLOCKS = 64: the
-    engine imbalance of head-major order shrinks like 1/NB, and at long
-    contexts the four K/V streams in flight cost more than it saves
-    (measured).
+    G heads.  G = BLOCK_MAJOR_HEADS = 4, or BLOCK_MAJOR_HEADS_SHORT = 16 when a
+    head has at most SHORT_HEAD_BLOCKS = 16 row blocks: short causal heads
+    finish their blocks quickly and a longer heavy-first prefix over more
+    heads balances the CUs better, while their K/V streams are short.  It
+    applies only when NB <= BLOCK_MAJOR_MAX_BLOCKS = 64: the engine imbalance
+    of head-major order shrinks like 1/NB, and at long contexts the K/V
+    streams in flight cost more than it saves (measured).
 """
 
 from __future__ import annotations
@@ -72,6 +75,8 @@ NAIVE_HEAD_FIRST = 1
 SWIZZLED_HEAD_FIRST = 2
 SWIZZLED_BLOCK_FIRST = 3
 BLOCK_MAJOR_HEADS = 4
+BLOCK_MAJOR_HEADS_SHORT = 16
+SHORT_HEAD_BLOCKS = 16
 BLOCK_MAJOR_MAX_BLOCKS = 64
 MAPPINGS = (NAIVE_BLOCK_FIRST, NAIVE_HEAD_FIRST, SWIZZLED_HEAD_FIRST, SWIZZLED_BLOCK_FIRST)
 
@@ -132,8 +137,9 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
         if xcd_block_major and NB <= BLOCK_MAJOR_MAX_BLOCKS and L0 % NB == 0 and n % NB == 0:
             hx = n // NB                       # whole heads in the piece
             k = L - L0                         # position within the XCD's sequence
-            first = (k // (BLOCK_MAJOR_HEADS * NB)) * BLOCK_MAJOR_HEADS
-            g = min(BLOCK_MAJOR_HEADS, hx - first)   # heads in k's group
+            G = BLOCK_MAJOR_HEADS_SHORT if NB <= SHORT_HEAD_BLOCKS else BLOCK_MAJOR_HEADS
+            first = (k // (G * NB)) * G        # first head of k's group
+            g = min(G, hx - first)             # heads in k's group
             j = k - first * NB                 # position within the group
             L = L0 + (first + j % g) * NB + j // g   # head j mod g, block j div g
         b, hq, m = unravel(L, (B, Hq, NB))

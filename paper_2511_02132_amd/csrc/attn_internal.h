@@ -46,8 +46,11 @@ constexpr int kQueueInts = 64;
 // Order bits (from ATTN_ORDER_HEAVY_FIRST and ATTN_ORDER_XCD_BLOCK_MAJOR).
 constexpr int kOrderHeavyFirst = 1;
 constexpr int kOrderXcdBlockMajor = 2;
-// Heads per block-major group: one per shader engine of an XCD.
+// Heads per block-major group: one per shader engine of an XCD; for heads of
+// at most kShortHeadBlocks row blocks, kBlockMajorHeadsShort.
 constexpr int kBlockMajorHeads = 4;
+constexpr int kBlockMajorHeadsShort = 16;
+constexpr int kShortHeadBlocks = 16;
 // Block-major groups apply only up to this many row blocks per head.
 constexpr int kBlockMajorMaxBlocks = 64;
 
@@ -66,17 +69,21 @@ constexpr int kBlockMajorMaxBlocks = 64;
 // Order bits:
 //  kOrderXcdBlockMajor (mapping 2 only): when XCD x's piece of the head-major
 //    order consists of whole heads (hx of them), the piece is cut into groups
-//    of kBlockMajorHeads consecutive heads (the last group may be smaller) and
-//    each group is dispatched block-major: within a group of g heads, its
+//    of G consecutive heads (the last group may be smaller) and each group is
+//    dispatched block-major: within a group of g heads, its
 //    j-th WG takes the group's head j mod g and block j div g.  Same tiles on
 //    the same XCD, different order inside the XCD.  The hardware hands an XCD
 //    its WGs in order, one per shader engine in turn (four per XCD); with this
 //    order four consecutive WGs cover one row block of four heads and cost the
 //    same under a causal mask, while the WGs in flight still share the K/V of
-//    only four heads.  Pieces that are not whole heads, and heads of more than
-//    kBlockMajorMaxBlocks row blocks, keep the head-major order: the engine
-//    imbalance that head-major order leaves is about 6/NB of the work, and at
-//    long contexts four K/V streams in flight cost more L2 hits than that.
+//    only four heads.  G = kBlockMajorHeads (4), or kBlockMajorHeadsShort (16)
+//    for heads of at most kShortHeadBlocks row blocks: such heads finish their
+//    blocks quickly, a heavy-first prefix over more heads balances the CUs
+//    better, and their K/V streams are short.  Pieces that are not whole
+//    heads, and heads of more than kBlockMajorMaxBlocks row blocks, keep the
+//    head-major order: the engine imbalance that head-major order leaves is
+//    about 6/NB of the work, and at long contexts four K/V streams in flight
+//    cost more L2 hits than that.
 //  kOrderHeavyFirst then replaces m by NB-1-m: the XCD of every (b, hq) is
 //    unchanged, but each head's row blocks are dispatched from the last (under
 //    a causal mask the most expensive) to the first.
@@ -111,9 +118,10 @@ __host__ __device__ inline Tile map_wid(int mapping, int order, int wid, int B, 
         if ((order & kOrderXcdBlockMajor) != 0 && NB <= kBlockMajorMaxBlocks && L0 % NB == 0 &&
             nx % NB == 0) {
             const int hx = nx / NB;
-            const int span = kBlockMajorHeads * NB;
-            const int g0 = (k / span) * kBlockMajorHeads;   // first local head of k's group
-            const int g = (hx - g0 < kBlockMajorHeads) ? hx - g0 : kBlockMajorHeads;
+            const int G = NB <= kShortHeadBlocks ? kBlockMajorHeadsShort : kBlockMajorHeads;
+            const int span = G * NB;
+            const int g0 = (k / span) * G;   // first local head of k's group
+            const int g = (hx - g0 < G) ? hx - g0 : G;
             const int j = k - g0 * NB;
             L = L0 + (g0 + j % g) * NB + j / g;
         } else {

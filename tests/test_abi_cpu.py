@@ -102,7 +102,8 @@ def test_stream_roundtrip():
 MAP_SHAPES = [(1, 4, 256, 64, 8), (1, 32, 8192, 128, 8), (1, 64, 8192, 128, 8),
               (8, 64, 4096, 128, 8), (1, 16, 131072, 128, 8), (2, 12, 300, 128, 8),
               (3, 5, 1000, 64, 4), (1, 1, 1, 128, 8), (2, 3, 129, 64, 1), (1, 8, 16384, 128, 8),
-              (1, 128, 8192, 56, 8)]
+              (1, 128, 8192, 56, 8), (1, 128, 2048, 56, 8), (2, 128, 2048, 128, 8),
+              (1, 64, 2176, 64, 8)]
 
 
 @pytest.mark.parametrize("B,Hq,Sq,d,NX", MAP_SHAPES)

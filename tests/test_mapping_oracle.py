@@ -166,7 +166,9 @@ def pin_xcd_block_major(m):
     for (B, Hq, NB, NX) in SHAPES[::3] + [(1, 32, 32, 8), (1, 64, 32, 8), (8, 64, 16, 8),
                                           (1, 16, 512, 8), (2, 12, 3, 8), (1, 128, 16, 8),
                                           (2, 128, 8, 8), (1, 48, 5, 8), (3, 40, 4, 8),
-                                          (1, 16, 64, 8), (1, 16, 65, 8), (1, 32, 128, 8)]:
+                                          (1, 16, 64, 8), (1, 16, 65, 8), (1, 32, 128, 8),
+                                          (1, 128, 16, 8), (2, 72, 16, 8), (1, 64, 17, 8),
+                                          (1, 64, 15, 8)]:
         N = B * Hq * NB
         for heavy in (False, True):
             plain = _table(m, mp.SWIZZLED_HEAD_FIRST, B, Hq, NB, NX) if not heavy else \
@@ -185,11 +187,13 @@ def pin_xcd_block_major(m):
                     continue
                 if NB <= 64 and L0 % NB == 0 and n % NB == 0:
                     hx = n // NB
-                    # the expected order, built by nested loops: groups of four
-                    # local heads in turn, each group block-major
+                    # the expected order, built by nested loops: groups of G
+                    # local heads in turn (16 for heads of at most 16 row
+                    # blocks, else 4), each group block-major
+                    G = 16 if NB <= 16 else 4
                     want = []
-                    for g0 in range(0, hx, 4):
-                        group = range(g0, min(g0 + 4, hx))
+                    for g0 in range(0, hx, G):
+                        group = range(g0, min(g0 + G, hx))
                         for blk in range(NB):
                             for h in group:
                                 want.append((h, blk))
@@ -197,12 +201,12 @@ def pin_xcd_block_major(m):
                     heads = seq[:, 0] * Hq + seq[:, 1]
                     got = list(zip((heads - L0 // NB).tolist(), blocks.tolist()))
                     assert got == want, (B, Hq, NB, NX, x)
-                    # four consecutive WGs of a full group share a row block
-                    full = (hx // 4) * 4 * NB
-                    assert all(len(set(blocks[i:i + 4])) == 1 for i in range(0, full, 4))
-                    # at most four heads among any 4*NB consecutive WGs of a group
-                    for i in range(0, n, 4 * NB):
-                        assert len(set(heads[i:i + 4 * NB].tolist())) <= 4
+                    # G consecutive WGs of a full group share a row block
+                    full = (hx // G) * G * NB
+                    assert all(len(set(blocks[i:i + G])) == 1 for i in range(0, full, G))
+                    # at most G heads among any G*NB consecutive WGs of a group
+                    for i in range(0, n, G * NB):
+                        assert len(set(heads[i:i + G * NB].tolist())) <= G
                 else:
                     assert np.array_equal(seq, plain[sel])
     with pytest.raises(ValueError):
@@ -296,10 +300,12 @@ class _Mutant:
         self.__dict__.setdefault("bm_rank", _bm_rank)
 
 
-def _bm_rank(L, x, N, NX, NB, G=4, max_blocks=64):
+def _bm_rank(L, x, N, NX, NB, G=4, max_blocks=64, G_short=16, short_blocks=16):
     L0, n = mp.xcd_piece(x, N, NX)
     if NB > max_blocks or L0 % NB or n % NB:
         return L
+    if NB <= short_blocks:
+        G = G_short
     hx = n // NB
     k = L - L0
     first = (k // (G * NB)) * G
@@ -387,6 +393,12 @@ MAP_MUTANTS = {
                                                                              max_blocks=1 << 30)),
     "block_major_limit_off_by_one": dict(bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB,
                                                                                 max_blocks=63)),
+    "block_major_short_heads_in_fours": dict(
+        bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB, G_short=4)),
+    "block_major_short_limit_above": dict(
+        bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB, short_blocks=17)),
+    "block_major_short_limit_below": dict(
+        bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB, short_blocks=15)),
     "block_first_swizzle_transposed": dict(
         sbf_head=lambda j, Hq, NX: (j % (Hq // NX if Hq >= NX else 1)) * NX + j // max(Hq // NX, 1)
         if Hq % NX == 0 else j),
