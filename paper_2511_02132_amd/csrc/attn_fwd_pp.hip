@@ -25,7 +25,9 @@
 //
 // LDS: kStages stages of 32 KiB, stage j = {K(j+1), V(j)}, read in phases
 // 2j+1 (A) and 2j+2 (B) and copied global -> LDS (buffer_load ... lds) kAhead
-// stages ahead; optionally (kQInLds) the block's Q rows as well.
+// stages ahead, inside the loop by group B alone, during its softmax step, so
+// that group A's product step starts on MFMAs; optionally (kQInLds) the
+// block's Q rows as well.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -105,14 +107,9 @@ __device__ __forceinline__ void gemm_schedule_impl() {
     gemm_schedule_step<PF, 0>();
 }
 
-// Wait until at most 4*n copy instructions (the n newest stages) are in flight.
-__device__ __forceinline__ void wait_copies(const int n) {
-    if (n <= 0)
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    else if (n == 1)
-        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else
-        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+// Wait until every copy this wave issued has landed in LDS.
+__device__ __forceinline__ void wait_copies() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // LDS of one workgroup: kStages stages of a K and a V tile (64 x 128 bf16),
@@ -123,7 +120,11 @@ constexpr int kPPLdsBytes = kStages * 2 * kBlockN * 256 + (kQInLds ? kBlockM128 
 // workgroup id `wid` (decoded by the mapping), with the LDS at `smem`.  It
 // starts and ends with every wave at the same barrier count, so a persistent
 // workgroup can run it repeatedly.
-template <bool CAUSAL, int MAPPING, int ORDER>
+// B_COPIES: inside the loop group B issues every copy of a stage (the
+// dispatched kernel); otherwise each group copies its own share (the
+// persistent kernel, whose scalar registers are all in use: the extra LDS
+// addresses of the first scheme would spill).
+template <bool CAUSAL, int MAPPING, int ORDER, bool B_COPIES>
 __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char *smem) {
     constexpr int D = 128;
     constexpr int BM = kBlockM128;
@@ -175,10 +176,13 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
     // contiguous LDS bytes (lane j at 16*j); wave w fills slots
     // (w*IPW + i)*64 + lane of a tile, fetching the global chunk that the
     // swizzled layout puts there.
-    uint32_t k_src[IPW], v_src[IPW];
+    // Source offsets for this wave's slots (i < IPW) and, for a group-B wave,
+    // for those of wave w - 4 (i >= IPW), which group B copies inside the loop.
+    uint32_t k_src[2 * IPW], v_src[2 * IPW];
+    const int w_other = w >= 4 ? w - 4 : w;
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-        const int slot = (w * IPW + i) * 64 + lane;
+    for (int i = 0; i < 2 * IPW; ++i) {
+        const int slot = ((i < IPW ? w : w_other) * IPW + (i % IPW)) * 64 + lane;
         const int row = slot / CHUNKS_PER_ROW;
         const int phys = slot % CHUNKS_PER_ROW;
         k_src[i] = row * ROW_BYTES + ((phys ^ k_swizzle<D>(row)) * 16);
@@ -202,6 +206,20 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
 #pragma unroll
         for (int i = 0; i < IPW; ++i)
             lds_copy16(d, src[i], lds_base + dst + (w * IPW + i) * 1024);
+    };
+    // Tile n into both slot sets of a group-B wave (its own and wave w - 4's).
+    auto copy_tile_both = [&](const char *head, const uint32_t *src, const int n, const uint32_t dst) __attribute__((always_inline)) {
+        const uint32_t off = (uint32_t)n * TILE_BYTES;
+        const uint32_t left = off < kv_lim ? kv_lim - off : 0u;
+        const i32x4 d = buffer_words(head + (off < kv_lim ? off : 0u), left);
+#pragma unroll
+        for (int i = 0; i < 2 * IPW; ++i)
+            lds_copy16(d, src[i], lds_base + dst + ((i < IPW ? w : w_other) * IPW + (i % IPW)) * 1024);
+    };
+    auto copy_stage_both = [&](const int j) __attribute__((always_inline)) {
+        const uint32_t base = (uint32_t)(j % kStages) * STAGE_BYTES;
+        copy_tile_both(k_head, k_src, j + 1, base);
+        copy_tile_both(v_head, v_src, j, base + TILE_BYTES);
     };
     // Stage j = {K(j+1), V(j)} into buffer j % kStages.
     auto copy_stage = [&](const int j) __attribute__((always_inline)) {
@@ -424,22 +442,27 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
 
     // Every wave runs E(0) G(0) E(1) G(1) ... with a barrier after each step;
     // group B starts one barrier late (and group A ends with one extra), so
-    // the groups stay one phase apart.  Stage k+kAhead is copied at global
-    // phase 2k+1 -- by A before G(k), by B before E(k) -- into the buffer of
-    // stage k+kAhead-kStages, which both groups finished reading by phase 2k.
-    // Stage k is read from phase 2k+1 on, so every wave's share of it must
-    // have landed by the barrier that starts that phase.
+    // the groups stay one phase apart.  Stage k+1 is copied at global phase
+    // 2k+1 into the buffer of stage k-1, which both groups finished reading by
+    // phase 2k, and read from phase 2k+3 on.  With B_COPIES group B copies all
+    // of it before its E(k) (each B wave fills its own slots and those of the
+    // A wave on its SIMD), so A's product step starts on MFMAs; otherwise A
+    // copies its share before G(k) and B its share before E(k).  Each wave
+    // waits for its own copies before the barrier that ends phase 2k+2.
+    static_assert(kAhead == 1, "every wave waits for all of its copies one phase after issuing them");
     if (grp == 1) barrier_lds();
     auto tile = [&](const int k, auto buf_c) __attribute__((always_inline)) {
-        if (grp == 1 && k + kAhead < n_tiles) copy_stage(k + kAhead);
+        if (grp == 1 && k + 1 < n_tiles) {
+            if constexpr (B_COPIES) copy_stage_both(k + 1);
+            else copy_stage(k + 1);
+        }
         softmax_step(k);
-        // A, before its G(k): stage k has landed; stages up to k+kAhead-1 may fly.
-        if (grp == 0) wait_copies(min(kAhead - 1, n_tiles - 1 - k));
+        // A's share of stage k, copied during G(k-1)
+        if constexpr (!B_COPIES) if (grp == 0) wait_copies();
         barrier_lds();
-        if (grp == 0 && k + kAhead < n_tiles) copy_stage(k + kAhead);
+        if constexpr (!B_COPIES) if (grp == 0 && k + 1 < n_tiles) copy_stage(k + 1);
         gemm_step(k, buf_c);
-        // B, before A's G(k+1): stage k+1 has landed; up to k+kAhead may fly.
-        if (grp == 1) wait_copies(min(kAhead - 1, n_tiles - 2 - k));
+        if (grp == 1) wait_copies();
         barrier_lds();
     };
     // kStages tiles per trip, so that every LDS buffer offset is an immediate.
@@ -492,7 +515,7 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
 template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const KernelArgs p) {
     __shared__ __attribute__((aligned(1024))) char smem[kPPLdsBytes];
-    pp_tile<CAUSAL, MAPPING, ORDER>(p, blockIdx.x, smem);
+    pp_tile<CAUSAL, MAPPING, ORDER, true>(p, blockIdx.x, smem);
 }
 
 // Persistent form: one workgroup per CU takes tiles from per-XCD queues
@@ -538,7 +561,7 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_persistent_kernel(c
     while (cur >= 0) {
         int pending = 0;
         if (threadIdx.x == 0) pending = atomicAdd(&queue[x], 1);   // result needed at the end
-        pp_tile<CAUSAL, MAPPING, ORDER>(p, cur, smem);
+        pp_tile<CAUSAL, MAPPING, ORDER, false>(p, cur, smem);
         if (threadIdx.x == 0) next_wid = take(pending);
         __syncthreads();
         cur = next_wid;

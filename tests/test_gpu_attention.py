@@ -56,6 +56,7 @@ PROBE_SHAPES = [
     # B, Hq, Hkv, S, d
     (1, 4, 4, 256, 64), (1, 32, 32, 8192, 128), (1, 64, 8, 8192, 128), (8, 64, 64, 4096, 128),
     (1, 16, 16, 131072, 128), (2, 12, 4, 300, 128), (3, 5, 5, 1000, 64),
+    (2, 128, 128, 2048, 56),   # short heads: block-major groups of 16 heads
 ]
 
 
