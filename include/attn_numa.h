@@ -56,7 +56,8 @@ enum {
      * turn (four per XCD); under a causal mask this makes four consecutive
      * workgroups equally expensive (measured: head-major order left one
      * shader engine with 9% more work), while the workgroups in flight read
-     * the K/V of only four heads.  For heads of at most 16 row blocks the
+     * the K/V of only four heads.  For head dimension 56 and 64 (128-row
+     * blocks, four workgroups per CU) and heads of at most 16 row blocks the
      * groups hold 16 heads: short heads finish their blocks quickly and the
      * longer heavy-first prefix balances the compute units better (measured
      * +2 to +16% on 2K-token heads of 128-head prefill shapes), while their

@@ -57,10 +57,12 @@ Order options (not among the paper's mappings):
     dispatcher hands an XCD its WGs one per shader engine in turn, four shader
     engines per XCD (measured), so under a causal mask four consecutive WGs
     then cost the same, while the WGs in flight still read the K/V of only
-    G heads.  G = BLOCK_MAJOR_HEADS = 4, or BLOCK_MAJOR_HEADS_SHORT = 16 when a
-    head has at most SHORT_HEAD_BLOCKS = 16 row blocks: short causal heads
-    finish their blocks quickly and a longer heavy-first prefix over more
-    heads balances the CUs better, while their K/V streams are short.  It
+    G heads.  G = BLOCK_MAJOR_HEADS = 4, or, with ``short_head_groups`` (the
+    library sets it for its 128-row blocks, head dimension 56 and 64, four
+    workgroups per CU), BLOCK_MAJOR_HEADS_SHORT = 16 when a head has at most
+    SHORT_HEAD_BLOCKS = 16 row blocks: short causal heads finish their blocks
+    quickly and a longer heavy-first prefix over more heads balances the CUs
+    better, while such heads' K/V streams are short.  It
     applies only when NB <= BLOCK_MAJOR_MAX_BLOCKS = 64: the engine imbalance
     of head-major order shrinks like 1/NB, and at long contexts the K/V
     streams in flight cost more than it saves (measured).
@@ -120,7 +122,8 @@ def xcd_piece(x: int, N: int, NX: int) -> tuple:
 
 
 def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
-            heavy_first: bool = False, xcd_block_major: bool = False) -> tuple:
+            heavy_first: bool = False, xcd_block_major: bool = False,
+            short_head_groups: bool = False) -> tuple:
     """(b, hq, m) that WG ``wid`` computes under ``mapping``."""
     N = B * Hq * NB
     if not 0 <= wid < N:
@@ -137,7 +140,8 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
         if xcd_block_major and NB <= BLOCK_MAJOR_MAX_BLOCKS and L0 % NB == 0 and n % NB == 0:
             hx = n // NB                       # whole heads in the piece
             k = L - L0                         # position within the XCD's sequence
-            G = BLOCK_MAJOR_HEADS_SHORT if NB <= SHORT_HEAD_BLOCKS else BLOCK_MAJOR_HEADS
+            G = BLOCK_MAJOR_HEADS_SHORT if short_head_groups and NB <= SHORT_HEAD_BLOCKS \
+                else BLOCK_MAJOR_HEADS
             first = (k // (G * NB)) * G        # first head of k's group
             g = min(G, hx - first)             # heads in k's group
             j = k - first * NB                 # position within the group
@@ -154,13 +158,15 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
 
 
 def enumerate_mapping(mapping: int, B: int, Hq: int, Sq: int, BM: int, NX: int,
-                      heavy_first: bool = False, xcd_block_major: bool = False) -> np.ndarray:
+                      heavy_first: bool = False, xcd_block_major: bool = False,
+                      short_head_groups: bool = False) -> np.ndarray:
     """Array [N, 3] of (b, hq, m) for wid = 0 .. N-1 (pure-Python loop)."""
     NB = num_row_blocks(Sq, BM)
     N = B * Hq * NB
     out = np.empty((N, 3), dtype=np.int64)
     for wid in range(N):
-        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX, heavy_first, xcd_block_major)
+        out[wid] = map_wid(mapping, wid, B, Hq, NB, NX, heavy_first, xcd_block_major,
+                           short_head_groups)
     return out
 
 

@@ -279,9 +279,11 @@ int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *o
     if (n < 0) return (int)n;
     if (n > INT32_MAX) return ATTN_ERR_SHAPE;
     const int nb = (Sq + attn::block_m_for(d) - 1) / attn::block_m_for(d);
+    // the four-wave kernel (128-row blocks) uses the 16-head groups for short heads
+    const bool short_groups = attn::block_m_for(d) == attn::kBlockM;
     for (int64_t wid = 0; wid < n; ++wid) {
         const attn::Tile t = attn::map_wid(mapping & 0xf, order_bits(mapping),
-                                           (int)wid, B, Hq, nb, NX);
+                                           (int)wid, B, Hq, nb, NX, short_groups);
         out[3 * wid + 0] = t.b;
         out[3 * wid + 1] = t.hq;
         out[3 * wid + 2] = t.m;

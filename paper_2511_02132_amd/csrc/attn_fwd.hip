@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const KernelArgs 
     const int c = lane & 31;   // query column of the MFMA tiles
     const int h = lane >> 5;   // which half of the 64 lanes
 
-    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NB, p.NX);
+    const Tile t = map_wid(MAPPING, ORDER, blockIdx.x, p.B, p.Hq, p.NB, p.NX, true);
     if (p.probe != nullptr && tid == 0) {
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));

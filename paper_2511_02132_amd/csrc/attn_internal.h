@@ -76,10 +76,13 @@ constexpr int kBlockMajorMaxBlocks = 64;
 //    its WGs in order, one per shader engine in turn (four per XCD); with this
 //    order four consecutive WGs cover one row block of four heads and cost the
 //    same under a causal mask, while the WGs in flight still share the K/V of
-//    only four heads.  G = kBlockMajorHeads (4), or kBlockMajorHeadsShort (16)
-//    for heads of at most kShortHeadBlocks row blocks: such heads finish their
-//    blocks quickly, a heavy-first prefix over more heads balances the CUs
-//    better, and their K/V streams are short.  Pieces that are not whole
+//    only four heads.  G = kBlockMajorHeads (4), or, with short_groups (set for
+//    the 128-row blocks of head dimension 56 and 64, four WGs per CU),
+//    kBlockMajorHeadsShort (16) for heads of at most kShortHeadBlocks row
+//    blocks: such heads finish their blocks quickly, a heavy-first prefix over
+//    more heads balances the CUs better, and their K/V streams are short.  (At
+//    d = 128 a head of 16 row blocks streams 2 MiB of K/V and 16 of them
+//    overflow the L2.)  Pieces that are not whole
 //    heads, and heads of more than kBlockMajorMaxBlocks row blocks, keep the
 //    head-major order: the engine imbalance that head-major order leaves is
 //    about 6/NB of the work, and at long contexts four K/V streams in flight
@@ -88,7 +91,8 @@ constexpr int kBlockMajorMaxBlocks = 64;
 //    unchanged, but each head's row blocks are dispatched from the last (under
 //    a causal mask the most expensive) to the first.
 __host__ __device__ inline Tile map_wid(int mapping, int order, int wid, int B, int Hq,
-                                        int NB, int NX) {
+                                        int NB, int NX,
+                                        bool short_groups = false) {
     const bool heavy_first = (order & kOrderHeavyFirst) != 0;
     Tile t;
     if (mapping == 0 || mapping == 3) {
@@ -118,7 +122,8 @@ __host__ __device__ inline Tile map_wid(int mapping, int order, int wid, int B, 
         if ((order & kOrderXcdBlockMajor) != 0 && NB <= kBlockMajorMaxBlocks && L0 % NB == 0 &&
             nx % NB == 0) {
             const int hx = nx / NB;
-            const int G = NB <= kShortHeadBlocks ? kBlockMajorHeadsShort : kBlockMajorHeads;
+            const int G = (short_groups && NB <= kShortHeadBlocks) ? kBlockMajorHeadsShort
+                                                                  : kBlockMajorHeads;
             const int span = G * NB;
             const int g0 = (k / span) * G;   // first local head of k's group
             const int g = (hx - g0 < G) ? hx - g0 : G;

@@ -113,6 +113,7 @@ def test_library_mapping_equals_oracle(B, Hq, Sq, d, NX):
         mapping, heavy, xbm = mp.split_flags(value)
         got = pa.map_tiles(value, B, Hq, Sq, d, NX)
         want = mp.enumerate_mapping(mapping, B, Hq, Sq, BM, NX, heavy_first=heavy,
+                                    short_head_groups=(BM == 128),
                                     xcd_block_major=xbm)
         assert np.array_equal(got, want), hex(value)
 

@@ -76,6 +76,7 @@ def test_probe_matches_enumeration_and_dispatch(B, Hq, Hkv, S, d):
         torch.cuda.synchronize()
         rec = probe.cpu().numpy()
         want = mp.enumerate_mapping(mapping, B, Hq, S, BM, nx, heavy_first=heavy,
+                                    short_head_groups=(BM == 128),
                                     xcd_block_major=xbm)
         assert np.array_equal(rec[:, :3], want), "placement differs from the enumeration"
         wid = np.arange(rec.shape[0])

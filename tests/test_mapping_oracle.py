@@ -170,11 +170,11 @@ def pin_xcd_block_major(m):
                                           (1, 128, 16, 8), (2, 72, 16, 8), (1, 64, 17, 8),
                                           (1, 64, 15, 8)]:
         N = B * Hq * NB
-        for heavy in (False, True):
+        for heavy, short in ((False, False), (True, False), (True, True)):
             plain = _table(m, mp.SWIZZLED_HEAD_FIRST, B, Hq, NB, NX) if not heavy else \
                 np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, True)
                           for w in range(N)])
-            bm = np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, heavy, True)
+            bm = np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, heavy, True, short)
                            for w in range(N)])
             keys = (bm[:, 0] * Hq + bm[:, 1]) * NB + bm[:, 2]
             assert np.array_equal(np.sort(keys), np.arange(N))       # a permutation
@@ -189,8 +189,9 @@ def pin_xcd_block_major(m):
                     hx = n // NB
                     # the expected order, built by nested loops: groups of G
                     # local heads in turn (16 for heads of at most 16 row
-                    # blocks, else 4), each group block-major
-                    G = 16 if NB <= 16 else 4
+                    # blocks when short-head groups are asked for, else 4),
+                    # each group block-major
+                    G = 16 if short and NB <= 16 else 4
                     want = []
                     for g0 in range(0, hx, G):
                         group = range(g0, min(g0 + G, hx))
@@ -272,7 +273,8 @@ class _Mutant:
         # map_wid must see the replaced helpers
         me = self
 
-        def map_wid(mapping, wid, B, Hq, NB, NX, heavy_first=False, xcd_block_major=False):
+        def map_wid(mapping, wid, B, Hq, NB, NX, heavy_first=False, xcd_block_major=False,
+                    short_head_groups=False):
             N = B * Hq * NB
             if not 0 <= wid < N:
                 raise ValueError("wid out of range")
@@ -288,7 +290,7 @@ class _Mutant:
             else:
                 L = me.swizzled_rank(wid, N, NX)
                 if xcd_block_major:
-                    L = me.bm_rank(L, wid % NX, N, NX, NB)
+                    L = me.bm_rank(L, wid % NX, N, NX, NB, short_head_groups)
                 b, hq, mm = me.unravel(L, (B, Hq, NB))
             if heavy_first:
                 mm = me.reverse_block(mm, NB)
@@ -300,11 +302,12 @@ class _Mutant:
         self.__dict__.setdefault("bm_rank", _bm_rank)
 
 
-def _bm_rank(L, x, N, NX, NB, G=4, max_blocks=64, G_short=16, short_blocks=16):
+def _bm_rank(L, x, N, NX, NB, short=False, G=4, max_blocks=64, G_short=16, short_blocks=16,
+             ignore_flag=False):
     L0, n = mp.xcd_piece(x, N, NX)
     if NB > max_blocks or L0 % NB or n % NB:
         return L
-    if NB <= short_blocks:
+    if (short or ignore_flag) and NB <= short_blocks:
         G = G_short
     hx = n // NB
     k = L - L0
@@ -314,7 +317,7 @@ def _bm_rank(L, x, N, NX, NB, G=4, max_blocks=64, G_short=16, short_blocks=16):
     return L0 + (first + j % g) * NB + j // g
 
 
-def _bm_rank_whole_piece(L, x, N, NX, NB):
+def _bm_rank_whole_piece(L, x, N, NX, NB, short=False):
     """Block-major across all heads of the piece (no groups)."""
     L0, n = mp.xcd_piece(x, N, NX)
     if NB > 64 or L0 % NB or n % NB:
@@ -324,7 +327,7 @@ def _bm_rank_whole_piece(L, x, N, NX, NB):
     return L0 + (k % hx) * NB + k // hx
 
 
-def _bm_rank_transposed(L, x, N, NX, NB):
+def _bm_rank_transposed(L, x, N, NX, NB, short=False):
     L0, n = mp.xcd_piece(x, N, NX)
     if NB > 64 or L0 % NB or n % NB:
         return L
@@ -336,7 +339,7 @@ def _bm_rank_transposed(L, x, N, NX, NB):
     return L0 + first * NB + (j // NB) + (j % NB) * g if g == NB else L0 + first * NB + j
 
 
-def _bm_rank_any_piece(L, x, N, NX, NB):
+def _bm_rank_any_piece(L, x, N, NX, NB, short=False):
     L0, n = mp.xcd_piece(x, N, NX)
     if NB > 64:
         return L
@@ -348,7 +351,7 @@ def _bm_rank_any_piece(L, x, N, NX, NB):
     return L0 + (first + j % g) * NB + j // g
 
 
-def _bm_rank_full_last_group(L, x, N, NX, NB):
+def _bm_rank_full_last_group(L, x, N, NX, NB, short=False):
     """Treats a short last group as four heads wide."""
     L0, n = mp.xcd_piece(x, N, NX)
     if NB > 64 or L0 % NB or n % NB:
@@ -389,16 +392,18 @@ MAP_MUTANTS = {
     "block_major_on_partial_pieces": dict(bm_rank=_bm_rank_any_piece),
     "block_major_whole_piece": dict(bm_rank=_bm_rank_whole_piece),
     "block_major_full_last_group": dict(bm_rank=_bm_rank_full_last_group),
-    "block_major_at_any_length": dict(bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB,
-                                                                             max_blocks=1 << 30)),
-    "block_major_limit_off_by_one": dict(bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB,
-                                                                                max_blocks=63)),
-    "block_major_short_heads_in_fours": dict(
-        bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB, G_short=4)),
-    "block_major_short_limit_above": dict(
-        bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB, short_blocks=17)),
-    "block_major_short_limit_below": dict(
-        bm_rank=lambda L, x, N, NX, NB: _bm_rank(L, x, N, NX, NB, short_blocks=15)),
+    "block_major_at_any_length": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
+        L, x, N, NX, NB, sh, max_blocks=1 << 30)),
+    "block_major_limit_off_by_one": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
+        L, x, N, NX, NB, sh, max_blocks=63)),
+    "block_major_short_heads_in_fours": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
+        L, x, N, NX, NB, sh, G_short=4)),
+    "block_major_short_limit_above": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
+        L, x, N, NX, NB, sh, short_blocks=17)),
+    "block_major_short_limit_below": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
+        L, x, N, NX, NB, sh, short_blocks=15)),
+    "block_major_short_groups_always": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
+        L, x, N, NX, NB, sh, ignore_flag=True)),
     "block_first_swizzle_transposed": dict(
         sbf_head=lambda j, Hq, NX: (j % (Hq // NX if Hq >= NX else 1)) * NX + j // max(Hq // NX, 1)
         if Hq % NX == 0 else j),
