@@ -30,14 +30,42 @@ ARCH = "gfx950"
 KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_device.h", "attn_internal.h"]
 
 
+def code_tokens(text: str) -> str:
+    """C++ source without comments and with whitespace runs collapsed: what the
+    compiler sees, so an edit to a comment leaves the hash unchanged.  String
+    literals are kept as they are (a // or /* inside one is not a comment)."""
+    out = []
+    i, n = 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == '"' or c == "'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
-    """Short hash of the kernel sources: ties a counter summary to the code it measured."""
+    """Short hash of the kernel sources (comments and layout ignored): ties a
+    counter summary to the code it measured."""
     import hashlib
 
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(CSRC, name)) as f:
+            h.update(code_tokens(f.read()).encode())
     return h.hexdigest()[:16]
 
 

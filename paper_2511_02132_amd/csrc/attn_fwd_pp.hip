@@ -168,8 +168,9 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
         (void *)((char *)p.o + q_head * 2), 0, p.Sq * ROW_BYTES, kBufferFlags);
 
     // Q^T is the B operand of S^T = K Q^T: lane holds Q[row][16kk + 8h .. +7]
-    // for each k-step.  The block's Q rows stay in LDS (same swizzle as K)
-    // rather than in registers; each wave copies its own 32 rows.
+    // for each k-step, in registers (the default) or, with kQInLds, read from
+    // the block's Q rows in LDS (same swizzle as K; each wave copies its own
+    // 32 rows).
     const int q_wave0 = t.m * BM + 32 * w;
     const int my_q = q_wave0 + c;
     // Tile copies straight into LDS: each instruction of a wave fills 1024

@@ -172,3 +172,13 @@ def test_counter_summary_read_hit_bounds(tmp_path):
     assert swz["l2_read_hit_rate_bounds"] == [pytest.approx(0.7778, abs=1e-4),
                                               pytest.approx(0.8889, abs=1e-4)]
     assert swz["l2_requests_read_write_over_hit_miss"] == pytest.approx(1.0)
+
+
+def test_kernel_hash_ignores_comments_and_layout():
+    from paper_2511_02132_amd.build import code_tokens
+    a = 'int a = 1;  // one\n/* two\n */ const char *s = "x // y /* z */";\n'
+    b = 'int a = 1;\nconst char *s = "x // y /* z */";  // other words\n'
+    assert code_tokens(a) == code_tokens(b) == 'int a = 1; const char *s = "x // y /* z */";'
+    # code changes do change the tokens
+    assert code_tokens('int a = 2;') != code_tokens('int a = 1;')
+    assert code_tokens('char c = \'/\'; int d;') == "char c = '/'; int d;"
