@@ -182,3 +182,35 @@ def test_kernel_hash_ignores_comments_and_layout():
     # code changes do change the tokens
     assert code_tokens('int a = 2;') != code_tokens('int a = 1;')
     assert code_tokens('char c = \'/\'; int d;') == "char c = '/'; int d;"
+
+
+def test_sweep_l2_counters_forward_and_backward(tmp_path):
+    """Per-launch L2 hit rate and read-hit bounds from a sweep's counter run;
+    a backward call's dK/dV and dQ dispatches count as one launch."""
+    fwd = "void attn::(anonymous namespace)::attn_fwd_pp_kernel<true, 2, 3>(attn::KernelArgs)"
+    d = tmp_path / "fwd"
+    _write_counters(str(d), [
+        (1, fwd, 512 * 1024, "TCC_HIT", 900.0), (1, fwd, 512 * 1024, "TCC_MISS", 100.0),
+        (1, fwd, 512 * 1024, "TCC_READ", 950.0), (1, fwd, 512 * 1024, "TCC_WRITE", 50.0),
+    ])
+    cfg = {"B": 1, "Hq": 32, "Hkv": 32, "S": 8192}
+    man = tmp_path / "fwd.json"
+    man.write_text(json.dumps([{"config": cfg, "variant": pa.variant_name(0x32)}]))
+    key = (1, 32, 32, 8192, pa.variant_name(0x32))
+    assert sweep.l2_by_launch(str(d), str(man))[key] == pytest.approx(0.9)
+    lo, hi = sweep.l2_read_bounds_by_launch(str(d), str(man))[key]
+    assert lo == pytest.approx(850 / 950, abs=1e-4) and hi == pytest.approx(900 / 950, abs=1e-4)
+
+    # backward: the forward that made O and lse is dropped; dK/dV + dQ are summed
+    dkdv = "void attn::(anonymous namespace)::attn_bwd_dkdv_kernel<true, 2, 2>(attn::BwdArgs)"
+    dq = "void attn::(anonymous namespace)::attn_bwd_dq_kernel<true, 2, 3>(attn::BwdArgs)"
+    d = tmp_path / "bwd"
+    _write_counters(str(d), [
+        (1, fwd, 512 * 1024, "TCC_HIT", 1.0), (1, fwd, 512 * 1024, "TCC_MISS", 1.0),
+        (2, dkdv, 256 * 256, "TCC_HIT", 300.0), (2, dkdv, 256 * 256, "TCC_MISS", 100.0),
+        (3, dq, 256 * 256, "TCC_HIT", 500.0), (3, dq, 256 * 256, "TCC_MISS", 100.0),
+    ])
+    man = tmp_path / "bwd.json"
+    man.write_text(json.dumps([{"config": cfg, "variant": pa.variant_name(0x32)}]))
+    assert sweep.l2_by_launch(str(d), str(man))[key] == pytest.approx(0.8)   # 800 / 1000
+    assert sweep.l2_read_bounds_by_launch(str(d), str(man)) == {}            # no read counts
