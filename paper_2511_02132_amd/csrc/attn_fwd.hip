@@ -5,9 +5,10 @@
 // with the FlashAttention-2 partition of Section 2.3.1: one workgroup (WG) per
 // (batch b, query head hq, block m of BLOCK_M = 128 query rows), each WG
 // streaming every BLOCK_N = 64-key tile of its K/V head through LDS and
-// keeping an online-softmax state (running max, running sum, fp32
-// accumulator) per query row, rescaled whenever the running max grows (the
-// cross-tile "fix-up" of Section 2.3.1).  With GQA, query head hq reads K/V
+// keeping an online-softmax state (reference maximum, running sum, fp32
+// accumulator) per query row; the reference is raised, and the sum and
+// accumulator rescaled (the cross-tile "fix-up" of Section 2.3.1), only when
+// a tile's exponentials against it would grow too large.  With GQA, query head hq reads K/V
 // head hq / (Hq / Hkv).
 //
 // Placement (Sections 2.2, 3.2, 3.3): the hardware dispatches WG id `wid` to XCD
@@ -25,8 +26,9 @@
 //     block renumbered (the same XCD-major rank, within the row of Hq WGs) so
 //     that one XCD gets a contiguous range of heads -- a GQA group when the
 //     group count equals NX.
-// (map_wid in attn_internal.h.)  This kernel serves head dimension 64; head
-// dimension 128 runs the two-group kernel of attn_fwd_pp.hip.
+// (map_wid in attn_internal.h.)  This kernel serves head dimensions 64 and 56
+// (computed as 64 with zero columns); head dimension 128 runs the two-group
+// kernel of attn_fwd_pp.hip.
 //
 // Work split inside a WG (256 threads = 4 waves of 64 lanes, one per SIMD):
 // wave w owns query rows 32w..32w+31 of the block.  Both contractions use
@@ -38,8 +40,8 @@
 //   O^T (d x 32 queries) += V^T (d x 64 keys) * P^T (64 keys x 32)
 //     B operand = P from the S^T accumulator, converted to bf16 in place
 //     A operand = V columns, read with ds_read_b64_tr_b16 (transposing read)
-// so the softmax row reductions are lane-local except one exchange between
-// lanes l and l^32 per tile.
+// so the softmax row sums are lane-local; lanes l and l^32 add their halves
+// once, at the end (and exchange maxima only when the reference is raised).
 //
 // LDS (double-buffered K and V tiles, 2 x 2 x 64 x d bf16) is filled directly
 // by buffer loads (no register staging): the copy of tile n+1 runs while tile
