@@ -226,6 +226,8 @@ D56_SHAPES = [
     (2, 8, 2, 257, 300, False),
     (1, 4, 4, 1000, 1000, True),
     (1, 3, 3, 1, 1, False),
+    (1, 4, 2, 1, 777, False),       # one query row against a long ragged key range, GQA
+    (2, 6, 3, 130, 700, True),      # Sq < Skv under the top-left causal mask
 ]
 
 
