@@ -139,3 +139,33 @@ def test_calib_validation():
     assert lib.attn_calib_mfma(256, 4, R + 4, S) == -6      # int64 records: 8-byte aligned
     assert lib.attn_calib_mfma(256, 4, R, S + 2) == -6
     assert lib.attn_calib_mfma(256, 4, R, R + 8) == -8      # sink overlaps the records
+
+
+def test_header_is_c99_and_links_from_c(tmp_path):
+    """The boundary is a C ABI: a C99 program includes the header, links
+    against the library and calls host-only entry points (no GPU needed)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not installed")
+    src = tmp_path / "abi.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <string.h>\n#include "attn_numa.h"\n'
+        "int main(void) {\n"
+        "    int32_t t[3 * 8];\n"
+        "    if (attn_block_m(128) != 256 || attn_block_m(64) != 128) return 1;\n"
+        "    if (attn_block_n(56) != 64 || attn_block_m(96) != ATTN_ERR_UNSUPPORTED) return 2;\n"
+        "    if (attn_grid_size(1, 32, 8192, 128) != 1024) return 3;\n"
+        "    if (attn_map_tiles(ATTN_MAP_SWIZZLED_HEAD_FIRST, 1, 4, 256, 64, 8, t) != ATTN_OK) return 4;\n"
+        "    if (attn_fwd(0, 0, 0, 0, 1, 1, 1, 1, 1, 128, 0, 1.0f, 2) != ATTN_ERR_NULL) return 5;\n"
+        "    if (strlen(attn_strerror(ATTN_ERR_SHAPE)) == 0) return 6;\n"
+        '    printf("ok\\n");\n    return 0;\n}\n')
+    lib_dir = os.path.dirname(pa.LIB_PATH)
+    exe = tmp_path / "abi"
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                    "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                    "-L", lib_dir, "-lattn_numa", "-Wl,-rpath," + lib_dir],
+                   check=True, capture_output=True, text=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
