@@ -286,3 +286,79 @@ def test_planted_mistake_is_caught(tmp_path, name, pattern, repl):
         except (AssertionError, RuntimeError):
             caught.append(pin.__name__)
     assert caught, "planted mistake %s passed every pin" % name
+
+
+def test_oracle_c_under_address_and_ub_sanitizers(tmp_path):
+    """The C oracle (forward, sampled rows, row statistics, backward) on ragged
+    GQA shapes, built for the host with AddressSanitizer and UBSan: no
+    out-of-bounds access, leak or undefined behaviour, and finite results."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not installed")
+    here = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle")
+    drv = tmp_path / "drv.c"
+    drv.write_text(r'''
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+int oracle_attn_fwd_f64(const uint16_t*, const uint16_t*, const uint16_t*, double*, int, int, int,
+                        int, int, int, int, float, int);
+int oracle_attn_fwd_rows_f64(const uint16_t*, const uint16_t*, const uint16_t*, const int64_t*,
+                             int64_t, double*, int, int, int, int, int, int, int, float, int);
+int oracle_attn_bwd_f64(const uint16_t*, const uint16_t*, const uint16_t*, const uint16_t*,
+                        double*, double*, double*, int, int, int, int, int, int, int, float, int);
+int oracle_attn_row_stats_f64(const uint16_t*, const uint16_t*, const uint16_t*, const uint16_t*,
+                              const int64_t*, int64_t, double*, double*, int, int, int, int, int,
+                              int, int, float, int);
+static uint16_t *rnd(size_t n, unsigned s) {
+    uint16_t *p = malloc(n * sizeof *p);
+    for (size_t i = 0; i < n; ++i) { s = s * 1103515245u + 12345u; p[i] = 0x3c00 | (s >> 16 & 0x7f) | ((s >> 8) & 0x8000); }
+    return p;
+}
+static int finite(const double *x, size_t n) { for (size_t i = 0; i < n; ++i) if (!isfinite(x[i])) return 0; return 1; }
+int main(void) {
+    const int shapes[][7] = {{2, 4, 2, 5, 7, 8, 1}, {1, 3, 1, 9, 4, 16, 0}, {1, 2, 2, 1, 1, 8, 1}};
+    for (int c = 0; c < 3; ++c) {
+        const int B = shapes[c][0], Hq = shapes[c][1], Hkv = shapes[c][2], Sq = shapes[c][3];
+        const int Skv = shapes[c][4], d = shapes[c][5], causal = shapes[c][6];
+        const size_t nq = (size_t)B * Hq * Sq * d, nk = (size_t)B * Hkv * Skv * d;
+        uint16_t *q = rnd(nq, 1 + c), *k = rnd(nk, 2 + c), *v = rnd(nk, 3 + c), *dout = rnd(nq, 4 + c);
+        double *o = malloc(nq * sizeof *o), *dq = malloc(nq * sizeof *dq);
+        double *dk = malloc(nk * sizeof *dk), *dv = malloc(nk * sizeof *dv);
+        const int64_t nrows = (int64_t)B * Hq * Sq;
+        int64_t *rows = malloc((size_t)nrows * 3 * sizeof *rows);
+        for (int64_t r = 0; r < nrows; ++r) {
+            rows[3 * r] = r / ((int64_t)Hq * Sq); rows[3 * r + 1] = (r / Sq) % Hq; rows[3 * r + 2] = r % Sq;
+        }
+        double *orow = malloc((size_t)nrows * d * sizeof *orow), *lse = malloc((size_t)nrows * sizeof *lse);
+        double *dsum = malloc((size_t)nrows * sizeof *dsum);
+        const float sc = 0.35f;
+        if (oracle_attn_fwd_f64(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, sc, 1)) return 10 + c;
+        if (oracle_attn_fwd_rows_f64(q, k, v, rows, nrows, orow, B, Hq, Hkv, Sq, Skv, d, causal, sc, 1)) return 20 + c;
+        if (oracle_attn_row_stats_f64(q, k, v, dout, rows, nrows, lse, dsum, B, Hq, Hkv, Sq, Skv, d, causal, sc, 1)) return 30 + c;
+        if (oracle_attn_bwd_f64(q, k, v, dout, dq, dk, dv, B, Hq, Hkv, Sq, Skv, d, causal, sc, 1)) return 40 + c;
+        for (size_t i = 0; i < nq; ++i) if (fabs(o[i] - orow[i]) > 1e-12) return 50 + c;
+        if (!finite(o, nq) || !finite(lse, nrows) || !finite(dsum, nrows) || !finite(dq, nq) ||
+            !finite(dk, nk) || !finite(dv, nk)) return 60 + c;
+        free(q); free(k); free(v); free(dout); free(o); free(dq); free(dk); free(dv);
+        free(rows); free(orow); free(lse); free(dsum);
+    }
+    puts("ok");
+    return 0;
+}
+''')
+    exe = tmp_path / "drv"
+    cmd = [gcc, "-std=c11", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", "-Wno-unknown-pragmas", str(drv),
+           os.path.join(here, "attn_oracle.c"), os.path.join(here, "attn_bwd_oracle.c"),
+           "-o", str(exe), "-lm"]
+    b = subprocess.run(cmd, capture_output=True, text=True)
+    if b.returncode != 0 and "asan" in b.stderr.lower():
+        pytest.skip("sanitizer runtime not available: " + b.stderr[-200:])
+    assert b.returncode == 0, b.stderr[-2000:]
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120,
+                       env=dict(os.environ, ASAN_OPTIONS="detect_leaks=1"))
+    assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr[-2000:])
