@@ -107,6 +107,8 @@ SMALL = [
     (1, 3, 1, 64, 1000, 128, False),    # short q, long kv
     (3, 2, 2, 1000, 64, 64, True),
     (1, 16, 16, 1024, 1024, 128, True),
+    (1, 2, 2, 100, 128, 128, False),    # exactly two K/V tiles
+    (1, 2, 2, 190, 190, 128, True),     # three tiles, the last ragged (odd trip count)
 ]
 
 
