@@ -37,6 +37,7 @@ import os
 import re
 import statistics
 import sys
+import time
 
 MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
                  "swizzled_block_first"]
@@ -53,14 +54,14 @@ def variants(causal: bool):
     return pa.variants(causal)
 
 
-def configs(family: str, contexts, batches, heads):
+def configs(family: str, contexts, batches, heads, kv_heads=GQA_KV_HEADS):
     for S in contexts:
         for B in batches:
             for H in heads:
                 if family == "mha":
                     yield {"B": B, "Hq": H, "Hkv": H, "S": S}
                 else:
-                    yield {"B": B, "Hq": H, "Hkv": GQA_KV_HEADS, "S": S}
+                    yield {"B": B, "Hq": H, "Hkv": kv_heads, "S": S}
 
 
 def flops(c, causal, d=D):
@@ -75,10 +76,15 @@ def parse(argv=None):
     p.add_argument("--batches", type=int, nargs="+", default=list(BATCHES))
     p.add_argument("--heads", type=int, nargs="+", default=None,
                    help="query heads (default: the paper's list for the family)")
+    p.add_argument("--kv-heads", type=int, default=GQA_KV_HEADS,
+                   help="KV heads of the gqa family (1: one GPU's shard when heads are split by KV head)")
     p.add_argument("--non-causal", action="store_true")
     p.add_argument("--d", type=int, default=D, choices=(56, 64, 128), help="head dimension")
     p.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd")
     p.add_argument("--reps", type=int, default=2)
+    p.add_argument("--warmup-ms", type=float, default=1000.0,
+                   help="untimed launches for this long before the first configuration: the "
+                        "shader clock of a process's first few hundred milliseconds runs low")
     p.add_argument("--json", default=None, help="append one JSON line per configuration")
     p.add_argument("--profile", action="store_true")
     p.add_argument("--manifest", default=None)
@@ -108,7 +114,7 @@ def run(a):
     vs = variants(causal)
     manifest = []
     out = open(a.json, "a") if a.json else None
-    for ci, c in enumerate(configs(a.family, a.contexts, a.batches, a.heads)):
+    for ci, c in enumerate(configs(a.family, a.contexts, a.batches, a.heads, a.kv_heads)):
         gen.manual_seed(7919 * ci + 1)
         shape_q = (c["B"], c["Hq"], c["S"], a.d)
         shape_kv = (c["B"], c["Hkv"], c["S"], a.d)
@@ -132,9 +138,14 @@ def run(a):
             else:
                 pa.attn_fwd(q, k, v, o, causal=causal, scale=scale, mapping=m, stream=stream)
         if not a.profile:
-            # one untimed launch: the first launch on fresh buffers runs slow
-            launch(vs[0][1])
-            torch.cuda.synchronize()
+            # untimed launches: the first launch on fresh buffers runs slow, and
+            # the shader clock runs low early in a process (a time, not a count)
+            t_end = time.perf_counter() + (a.warmup_ms / 1e3 if ci == 0 else 0.0)
+            while True:
+                launch(vs[0][1])
+                torch.cuda.synchronize()
+                if time.perf_counter() >= t_end:
+                    break
         for _ in range(reps):
             for name, m in vs:
                 flush.zero_()

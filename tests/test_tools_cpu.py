@@ -214,3 +214,15 @@ def test_sweep_l2_counters_forward_and_backward(tmp_path):
     man.write_text(json.dumps([{"config": cfg, "variant": pa.variant_name(0x32)}]))
     assert sweep.l2_by_launch(str(d), str(man))[key] == pytest.approx(0.8)   # 800 / 1000
     assert sweep.l2_read_bounds_by_launch(str(d), str(man)) == {}            # no read counts
+
+
+def test_sweep_kv_heads_option():
+    from paper_2511_02132_amd import sweep
+    a = sweep.parse(["--family", "gqa", "--kv-heads", "1", "--heads", "8", "--contexts", "8192",
+                     "--batches", "1", "4"])
+    cs = list(sweep.configs(a.family, a.contexts, a.batches, a.heads, a.kv_heads))
+    assert cs == [{"B": 1, "Hq": 8, "Hkv": 1, "S": 8192}, {"B": 4, "Hq": 8, "Hkv": 1, "S": 8192}]
+    assert sweep.parse(["--family", "gqa"]).kv_heads == sweep.GQA_KV_HEADS
+    assert sweep.parse([]).warmup_ms == 1000.0
+    # the mha family ignores it: every q-head has its own KV head
+    assert [c["Hkv"] for c in sweep.configs("mha", [4096], [1], [16], 1)] == [16]
