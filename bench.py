@@ -1,14 +1,17 @@
 """Benchmark of the fused attention-forward hot path on one MI355X.
 
-A step is one attn_fwd call over the whole workload (default: MHA, B=1, H=32,
-S=8192, d=128, causal -- an 8B-class decoder layer) with the swizzled
-head-first mapping -- under a causal mask with two dispatch-order options that
-keep every head on its XCD: heavy-first blocks, and block-major order across
-the heads of each XCD's piece (so the four WGs an XCD receives at a time cost
-the same) -- inputs already resident in HBM.  Prints ONE JSON line:
+A step is one attn_fwd call over the whole workload (default: MHA, B=1, H=16,
+S=131072, d=128, causal -- the long-context case whose K/V per head, 64 MiB,
+far exceeds an XCD's 4 MB L2) with the swizzled head-first mapping -- under a
+causal mask with each head's row blocks dispatched heaviest first, which keeps
+every head on its XCD -- inputs already resident in HBM.  Prints ONE JSON line:
 
   value       attention TFLOP/s (FlashAttention flop convention) of the timed
-              K back-to-back steps
+              K back-to-back steps (warm: no cache flush between them), after
+              a warm-up of at least --warmup steps and --warmup-s seconds
+  headline_cold  the same variant launched alone after an L2 + MALL flush,
+              --reps times interleaved with the other variants: median, min,
+              max and IQR of the launch time
   roofline    the kernel against the dense bf16 MFMA peak (2.5 PFLOP/s):
               achieved = algorithmic flop per launch / average launch time
               (HIP events on the launch stream over the timed region);
@@ -24,15 +27,17 @@ the same) -- inputs already resident in HBM.  Prints ONE JSON line:
   per_mapping TFLOP/s of all four mappings (for causal workloads also each
               with the heavy-first block order) and of swizzled head-first with
               block-major order inside each XCD, interleaved, cold (L2 and MALL
-              flushed before every launch) and warm, median over reps, plus the
-              L2 hit rate from the counter summary
+              flushed before every launch) and warm, median over reps with min,
+              max and IQR, plus the L2 hit rate from the counter summary
+  small_workload  the small MHA case (B=1, H=4, S=256, d=64), which launch
+              latency bounds: every mapping, --small-reps interleaved cold
+              launches, median / min / IQR
   cpu_baseline  the fp64 CPU oracle on a time-bounded sample of the same
               workload's rows, in TFLOP/s of the same flop count
 
-The default warm-up (60 steps, about 30 ms of work at the default workload)
-outlasts the power manager's response to the start of a matrix-core load: the
-shader clock dips for some tens of milliseconds before it settles, and the K
-timed steps measure the settled rate.
+The warm-up is timed as well as counted: the power manager lowers the shader
+clock for some tens of milliseconds after a matrix-core load starts, and the
+K timed steps measure the settled rate.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
        python bench.py --profile [--workload NAME]   (kernel launches only, for rocprofv3)
@@ -49,7 +54,8 @@ import sys
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-DEFAULT_WORKLOAD = "mha_b1_h32_s8192_d128_causal"
+DEFAULT_WORKLOAD = "mha_b1_h16_s131072_d128_causal"
+SMALL_WORKLOAD = "mha_b1_h4_s256_d64"
 METRIC = "attention fwd TFLOP/s (% of bf16 MFMA peak) + L2 hit rate, per mapping"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
@@ -83,10 +89,15 @@ def counter_summary(workload: str):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=60)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--warmup-s", type=float, default=2.0,
+                   help="the warm-up also lasts at least this long (seconds)")
     p.add_argument("--workload", default=DEFAULT_WORKLOAD)
     p.add_argument("--reps", type=int, default=10, help="cold reps per mapping")
+    p.add_argument("--small-reps", type=int, default=300,
+                   help="cold reps per mapping of the small workload")
+    p.add_argument("--no-small", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--profile", action="store_true",
@@ -113,8 +124,8 @@ def main():
     B, Hq, Hkv, Sq, Skv, d, causal = (w[k] for k in ("B", "Hq", "Hkv", "Sq", "Skv", "d", "causal"))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    q, k, v = ai.workload_inputs(args.workload)
-    q, k, v = q.to(dev), k.to(dev), v.to(dev)
+    q_cpu, k_cpu, v_cpu = ai.workload_inputs(args.workload)
+    q, k, v = q_cpu.to(dev), k_cpu.to(dev), v_cpu.to(dev)
     o = torch.empty_like(q)
     scale = ai.default_scale(d)
     flops = pa.attention_flops(B, Hq, Sq, Skv, d, causal)
@@ -145,9 +156,15 @@ def main():
     # ---- headline: K back-to-back steps of the method (swizzled head-first)
     mapping = pa.method_variant(causal)
     headline_name = pa.variant_name(mapping)
-    for _ in range(args.warmup):
+    t_warm = time.perf_counter()
+    n_warm = 0
+    while n_warm < args.warmup or time.perf_counter() - t_warm < args.warmup_s:
         step(mapping)
+        n_warm += 1
+        if n_warm % 4 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
+    warm_s = time.perf_counter() - t_warm
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -160,8 +177,8 @@ def main():
     wall = time.perf_counter() - t0
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
     value = flops / (ms_per_step * 1e-3) / 1e12
-    print("headline: %.4f ms/step, %.1f TFLOP/s (wall %.3f s)" % (ms_per_step, value, wall),
-          file=sys.stderr, flush=True)
+    print("headline: %.4f ms/step, %.1f TFLOP/s (wall %.3f s; warm-up %d launches, %.2f s)"
+          % (ms_per_step, value, wall, n_warm, warm_s), file=sys.stderr, flush=True)
 
     # ---- compute ceiling: dense bf16 MFMA on register operands, after the
     # headline so that the clock has settled; the later half of the launches
@@ -177,37 +194,29 @@ def main():
     ceiling["frac_of_peak_at_clock"] = round(value / ceiling["peak_at_clock_tflops"], 4)
     print("mfma ceiling: %s" % json.dumps(ceiling), file=sys.stderr, flush=True)
 
-    # ---- per mapping: interleaved, cold (L2 + MALL flushed) and warm, median
+    # ---- per mapping: interleaved, cold (L2 + MALL flushed) and warm
     flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device=dev)
     vs = variants(causal)
-    cold = {n: [] for n, _ in vs}
-    warm = {n: [] for n, _ in vs}
-    for _ in range(args.reps):
-        for name, m in vs:
-            flush.zero_()
-            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-            e0.record(stream)
-            step(m)
-            e1.record(stream)
-            step(m)
-            e2.record(stream)
-            torch.cuda.synchronize()
-            cold[name].append(e0.elapsed_time(e1))
-            warm[name].append(e1.elapsed_time(e2))
-    del flush
+    cold, warm = timed_variants(torch, stream, flush, step, vs, args.reps, warm_too=True)
     counters = counter_summary(args.workload)
     per_mapping = {}
     for name, _ in vs:
-        cm, wm = statistics.median(cold[name]), statistics.median(warm[name])
-        ent = {"cold_ms": round(cm, 5), "cold_tflops": round(flops / cm / 1e9, 2),
-               "warm_ms": round(wm, 5), "warm_tflops": round(flops / wm / 1e9, 2),
-               "cold_ms_min": round(min(cold[name]), 5), "cold_ms_max": round(max(cold[name]), 5),
-               "cold_ms_iqr": round(float(np.subtract(*np.percentile(cold[name], [75, 25]))), 5)}
+        ent = {"cold": launch_stats(cold[name], flops), "warm": launch_stats(warm[name], flops)}
+        ent["cold_tflops"] = ent["cold"]["tflops_median"]
+        ent["warm_tflops"] = ent["warm"]["tflops_median"]
         if counters:
             c = counters["per_mapping"].get(name, {})
             ent["l2_hit_rate"] = c.get("l2_hit_rate")
         per_mapping[name] = ent
+    headline_cold = dict(per_mapping[headline_name]["cold"])
     print("per mapping: %s" % json.dumps(per_mapping), file=sys.stderr, flush=True)
+
+    # ---- the small workload: launch-latency bound, every mapping, many reps
+    small = None
+    if not args.no_small:
+        small = small_workload(args, torch, dev, stream, flush, ai, pa)
+        print("small workload: %s" % json.dumps(small), file=sys.stderr, flush=True)
+    del flush
 
     # ---- roofline of the kernel (MFMA-bound contraction, bf16 peak)
     achieved = flops / (ms_per_step * 1e-3) / 1e12
@@ -217,29 +226,100 @@ def main():
         traffic = t.get("hbm_bytes_per_launch")
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic}
+                "traffic": traffic,
+                "work_per_launch": "%.6g flop = 4*B*Hq*Sq*Skv*d%s" % (
+                    flops, " / 2 (causal)" if causal else "")}
 
     # ---- CPU baseline: the oracle on a time-bounded sample of rows
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, w, q, k, v, scale)
+        cpu = cpu_baseline(args, w, q_cpu, k_cpu, v_cpu, scale)
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "steps": args.steps, "warmup": n_warm, "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic: Q,K,V ~ N(0,1) rounded to bf16, seeded",
+        "timing": "value: K back-to-back launches (warm) after a warm-up of %d launches "
+                  "(%.2f s); headline_cold: the same variant after an L2 + MALL flush, %d "
+                  "interleaved reps" % (n_warm, warm_s, args.reps),
         "config": {"workload": args.workload, "B": B, "Hq": Hq, "Hkv": Hkv, "Sq": Sq, "Skv": Skv,
                    "d": d, "causal": causal, "mapping": headline_name,
                    "block_m": pa.block_m(d), "block_n": pa.block_n(d), "num_xcd": pa.num_xcd(),
                    "flop_convention": "4*B*Hq*Sq*Skv*d, halved when causal"},
         "roofline": roofline,
+        "headline_cold": headline_cold,
         "mfma_ceiling": ceiling,
         "per_mapping": per_mapping,
+        "small_workload": small,
         "cpu_baseline": cpu,
         "kernel_source_sha256": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)
+
+
+def timed_variants(torch, stream, flush, step, vs, reps, warm_too=False):
+    """Launch times (ms) of every variant, interleaved round-robin over reps:
+    cold = one launch right after an L2 + MALL flush; warm = the launch that
+    follows it (same inputs, caches as the cold launch left them)."""
+    cold = {n: [] for n, _ in vs}
+    warm = {n: [] for n, _ in vs}
+    for _ in range(reps):
+        for name, m in vs:
+            flush.zero_()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record(stream)
+            step(m)
+            e[1].record(stream)
+            if warm_too:
+                step(m)
+                e[2].record(stream)
+            torch.cuda.synchronize()
+            cold[name].append(e[0].elapsed_time(e[1]))
+            if warm_too:
+                warm[name].append(e[1].elapsed_time(e[2]))
+    return cold, warm
+
+
+def launch_stats(ms, flops):
+    """Median, min, max and interquartile range of launch times (ms), and the
+    median and best rate in TFLOP/s."""
+    import numpy as np
+    med = float(np.median(ms))
+    q75, q25 = np.percentile(ms, [75, 25])
+    return {"n": len(ms), "ms_median": round(med, 5), "ms_min": round(float(min(ms)), 5),
+            "ms_max": round(float(max(ms)), 5), "ms_iqr": round(float(q75 - q25), 5),
+            "tflops_median": round(flops / med / 1e9, 2),
+            "tflops_best": round(flops / float(min(ms)) / 1e9, 2)}
+
+
+def small_workload(args, torch, dev, stream, flush, ai, pa):
+    """Every mapping on the small MHA workload (B1 H4 S256 d64, non-causal):
+    launch-latency bound, so many interleaved cold reps."""
+    w = ai.WORKLOADS[SMALL_WORKLOAD]
+    qs, ks, vs_ = (t.to(dev) for t in ai.workload_inputs(SMALL_WORKLOAD))
+    os_ = torch.empty_like(qs)
+    sc = ai.default_scale(w["d"])
+    fl = pa.attention_flops(w["B"], w["Hq"], w["Sq"], w["Skv"], w["d"], w["causal"])
+
+    def st(m):
+        pa.attn_fwd(qs, ks, vs_, os_, causal=w["causal"], scale=sc, mapping=m, stream=stream)
+
+    vs = variants(w["causal"])
+    for _, m in vs:   # one untimed launch each
+        st(m)
+    torch.cuda.synchronize()
+    cold, _ = timed_variants(torch, stream, flush, st, vs, args.small_reps)
+    out = {"workload": SMALL_WORKLOAD, "flop": fl, "reps": args.small_reps,
+           "note": "one launch of 8 workgroups; bound by launch latency, not by the MFMA rate",
+           "per_mapping": {}}
+    for name, _ in vs:
+        st_ = launch_stats(cold[name], fl)
+        out["per_mapping"][name] = {"us_median": round(st_["ms_median"] * 1e3, 2),
+                                    "us_min": round(st_["ms_min"] * 1e3, 2),
+                                    "us_iqr": round(st_["ms_iqr"] * 1e3, 2),
+                                    "tflops_median": st_["tflops_median"]}
+    return out
 
 
 def cpu_model() -> str:
@@ -261,7 +341,7 @@ def cpu_baseline(args, w, q, k, v, scale):
     import attn_inputs as ai
     import oracle
 
-    qb, kb, vb = (ai.bf16_bits(t.cpu()) for t in (q, k, v))
+    qb, kb, vb = (ai.bf16_bits(t) for t in (q, k, v))
     rng = np.random.default_rng(12345)
     total_flop, total_s, nrows = 0.0, 0.0, 0
     chunk = 64

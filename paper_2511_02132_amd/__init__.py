@@ -61,9 +61,10 @@ def variants(causal: bool):
 
 def method_variant(causal: bool) -> int:
     """The mapping value the headline uses: the paper's swizzled head-first
-    placement; under a causal mask with heavy-first, block-major dispatch."""
+    placement (each XCD serves one (batch, KV head) at a time); under a causal
+    mask each head's row blocks are dispatched heaviest first."""
     if causal:
-        return SWIZZLED_HEAD_FIRST | HEAVY_FIRST | XCD_BLOCK_MAJOR
+        return SWIZZLED_HEAD_FIRST | HEAVY_FIRST
     return SWIZZLED_HEAD_FIRST
 
 ATTN_OK = 0

@@ -1,7 +1,9 @@
 """GPU tests of the persistent form of the forward (attn_fwd_persistent, d = 128).
 
-All calls go through the C ABI.  The persistent form must produce bitwise the
-output of attn_fwd (same per-tile arithmetic), compute every tile exactly once
+All calls go through the C ABI.  The persistent form must match the fp64
+oracle (O within max-abs 2e-2 and mean-abs 2e-3, the row log-sum-exp within
+1e-4) on host-drawn seeded inputs for every mapping variant, produce bitwise
+the output of attn_fwd (same per-tile arithmetic), compute every tile exactly once
 (the probe, indexed by workgroup id, equals the CPU enumeration of the
 mapping), run each tile on the XCD its queue belongs to except for tiles taken
 from another queue at the end, and leave the queue buffer zeroed so that the
@@ -13,6 +15,7 @@ import pytest
 import torch
 
 import attn_inputs as ai
+import oracle
 import paper_2511_02132_amd as pa
 from oracle import mapping as mp
 
@@ -30,12 +33,92 @@ SHAPES = [
 ]
 
 
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+LSE_ABS = 1e-4   # d = 128: fp32 sum of fp32 exponentials (as attn_fwd_lse)
+
+
 def _inputs(B, Hq, Hkv, Sq, Skv, seed):
-    g = torch.Generator(device=DEV).manual_seed(seed)
-    q = torch.randn(B, Hq, Sq, 128, device=DEV, generator=g).to(torch.bfloat16)
-    k = torch.randn(B, Hkv, Skv, 128, device=DEV, generator=g).to(torch.bfloat16)
-    v = torch.randn(B, Hkv, Skv, 128, device=DEV, generator=g).to(torch.bfloat16)
-    return q, k, v
+    return [t.to(DEV) for t in ai.make_qkv(B, Hq, Hkv, Sq, Skv, 128, seed_base=seed)]
+
+
+def _persistent(q, k, v, causal, scale, value, queue, probe=None):
+    B, Hq, Sq, _ = q.shape
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float32, device=DEV)
+    pa.attn_fwd_persistent(q, k, v, o, lse=lse, queue=queue, probe=probe, causal=causal,
+                           scale=scale, mapping=value)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def _check_rows(o, lse, qc, kc, vc, rows, causal, scale, what):
+    """O and lse rows of the persistent form against the oracle."""
+    qb, kb, vb = ai.bf16_bits(qc), ai.bf16_bits(kc), ai.bf16_bits(vc)
+    ref_o = oracle.attn_fwd_rows_f64(qb, kb, vb, rows, causal, scale)
+    ref_l, _ = oracle.attn_row_stats_f64(qb, kb, vb, None, rows, causal, scale)
+    oc = o.cpu()
+    got_o = oc[rows[:, 0], rows[:, 1], rows[:, 2]].float().numpy().astype(np.float64)
+    got_l = lse.cpu().numpy().astype(np.float64)[rows[:, 0], rows[:, 1], rows[:, 2]]
+    err = np.abs(got_o - ref_o)
+    assert not torch.isnan(oc).any(), (what, "unwritten output")
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (what, err.max(), err.mean())
+    assert np.abs(got_l - ref_l).max() <= LSE_ABS, (what, np.abs(got_l - ref_l).max())
+
+
+# Ragged GQA shapes with fewer tiles than compute units (at most 36 tiles of
+# 256 rows), plus the two persistent-test shapes that no other test checks
+# against the oracle.
+ORACLE_SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, causal
+    (1, 6, 2, 300, 450, True),
+    (2, 4, 1, 700, 513, False),
+    (1, 8, 4, 129, 1000, True),
+    (2, 12, 4, 700, 900, False),
+    (1, 64, 8, 2048, 2048, True),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Sq,Skv,causal", ORACLE_SHAPES)
+def test_persistent_matches_oracle(B, Hq, Hkv, Sq, Skv, causal):
+    """Every variant of the persistent form against the fp64 oracle: every row
+    on the small shapes, sampled rows (fixed boundary rows plus seeded random
+    ones per head) on the 2K GQA shape."""
+    print("persistent vs oracle", B, Hq, Hkv, Sq, Skv, causal, flush=True)
+    seed = 9300 + Sq + 7 * Skv
+    qc, kc, vc = ai.make_qkv(B, Hq, Hkv, Sq, Skv, 128, seed_base=seed)
+    q, k, v = qc.to(DEV), kc.to(DEV), vc.to(DEV)
+    scale = ai.default_scale(128)
+    if B * Hq * Sq <= 32768:
+        rows = oracle.all_rows(B, Hq, Sq)
+    else:
+        rows = ai.sample_rows(B, Hq, Sq, pa.block_m(128), 4, seed=seed)
+    queue = pa.new_queue(DEV)
+    ref = pa.attn_fwd(q, k, v, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    for value in VARIANTS:
+        o, lse = _persistent(q, k, v, causal, scale, value, queue)
+        _check_rows(o, lse, qc, kc, vc, rows, causal, scale, hex(value))
+        assert torch.equal(o, ref), hex(value)
+        assert int(queue.abs().sum()) == 0, "queue not reset by the last workgroup"
+
+
+def test_persistent_matches_oracle_8k_workload():
+    """The MHA B1 H32 8K causal workload with its own seeds: every variant of the
+    persistent form against the oracle on sampled rows (fixed boundary rows and
+    seeded random rows of every head)."""
+    name = "mha_b1_h32_s8192_d128_causal"
+    w = ai.WORKLOADS[name]
+    print("persistent vs oracle", name, flush=True)
+    qc, kc, vc = ai.workload_inputs(name)
+    q, k, v = qc.to(DEV), kc.to(DEV), vc.to(DEV)
+    scale = ai.default_scale(128)
+    rows = ai.sample_rows(w["B"], w["Hq"], w["Sq"], pa.block_m(128), 6, seed=w["index"])
+    queue = pa.new_queue(DEV)
+    for value in VARIANTS:
+        o, lse = _persistent(q, k, v, True, scale, value, queue)
+        _check_rows(o, lse, qc, kc, vc, rows, True, scale, hex(value))
+        assert int(queue.abs().sum()) == 0
 
 
 @pytest.mark.parametrize("B,Hq,Hkv,Sq,Skv,causal", SHAPES)

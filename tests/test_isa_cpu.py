@@ -72,11 +72,13 @@ def listings(tmp_path_factory):
 def _kernels(text: str):
     """(name, instruction lines) for every kernel body in a listing."""
     lines = text.splitlines()
+    # function symbols only (a device variable's label is data, not code)
+    funcs = set(re.findall(r"^\s*\.type\s+(\w+),@function", text, re.M))
     res = []
     i = 0
     while i < len(lines):
         m = re.match(r"^(_Z\w+):\s*(;.*)?$", lines[i])
-        if m:
+        if m and m.group(1) in funcs:
             name = m.group(1)
             body = []
             i += 1
