@@ -207,6 +207,33 @@ int attn_fwd_persistent(const void *q, const void *k, const void *v, void *o, fl
                         int32_t *queue, int32_t *probe, int B, int Hq, int Hkv, int Sq, int Skv,
                         int d, int causal, float scale, int mapping);
 
+/*
+ * attn_fwd_persistent_noalloc -- attn_fwd_persistent for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the tile queues live in a device array
+ * that the library owns instead of a caller buffer.  The call makes no
+ * hipMalloc, hipFree or other allocating call; the caller still provides q, k,
+ * v, o (and optionally lse and probe), with the meaning, layout and checks of
+ * attn_fwd_persistent.
+ *
+ * The array holds ATTN_QUEUE_INTS int32 (256 bytes) per GPU, for any grid;
+ * each GPU the library runs on keeps its copy until the process ends.  Its
+ * device address is looked up once per device, on the first call with that
+ * device current.  Each call first enqueues a one-workgroup kernel that zeroes
+ * the array, then the persistent kernel, both on the calling thread's stream;
+ * the array keeps the last call's contents (zero after a completed launch).
+ * Every call on one GPU shares that GPU's array: calls whose kernels may
+ * overlap on one GPU (different streams without ordering between them) race
+ * on it and may compute tiles twice or not at all; order them on one stream.
+ *
+ * Errors: as attn_fwd_persistent; ATTN_ERR_UNSUPPORTED for d != 128 or more
+ * than 32 XCDs (the array's maximum); ATTN_ERR_HIP if the array's address
+ * cannot be obtained.  The output is bitwise that of attn_fwd_persistent.
+ */
+int attn_fwd_persistent_noalloc(const void *q, const void *k, const void *v, void *o, float *lse,
+                                int32_t *probe, int B, int Hq, int Hkv, int Sq, int Skv,
+                                int d, int causal, float scale, int mapping);
+
 /* Number of workgroups attn_fwd launches: B * Hq * ceil(Sq / attn_block_m(d)),
  * or a negative ATTN_ERR_* code for an invalid shape. */
 int64_t attn_grid_size(int B, int Hq, int Sq, int d);

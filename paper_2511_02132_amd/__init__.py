@@ -83,6 +83,8 @@ SIGNATURES = {
                        _ci),
     "attn_fwd_lse": ([_vp, _vp, _vp, _vp, _vp, _ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_fwd_persistent": ([_vp] * 7 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
+    "attn_fwd_persistent_noalloc": ([_vp] * 6 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci],
+                                    _ci),
     "attn_bwd": ([_vp] * 10 + [_ci, _ci, _ci, _ci, _ci, _ci, _ci, _cf, _ci], _ci),
     "attn_calib_mfma": ([_ci, _ci, _vp, _vp], _ci),
     "attn_grid_size": ([_ci, _ci, _ci, _ci], ctypes.c_int64),
@@ -273,6 +275,33 @@ def attn_fwd_persistent(q, k, v, o=None, *, lse=None, queue=None, probe=None,
                                      B, Hq, Hkv, Sq, Skv, d, int(bool(causal)), scale,
                                      int(mapping)),
            "attn_fwd_persistent")
+    return o
+
+
+def attn_fwd_persistent_noalloc(q, k, v, o, *, lse=None, probe=None, causal: bool = False,
+                                scale: float | None = None, mapping: int = SWIZZLED_HEAD_FIRST,
+                                stream=None):
+    """attn_fwd_persistent on the library's own tile-queue array: the call
+    allocates nothing (o, and lse / probe when wanted, come from the caller).
+    Calls that may overlap on one GPU race on that array; order them on one
+    stream."""
+    import torch
+    if o is None:
+        raise ValueError("o must be given: this call allocates nothing")
+    o, (B, Hq, Hkv, Sq, Skv, d), scale = _prepare(q, k, v, o, scale, stream)
+    if lse is not None:
+        _check_stat(lse, (B, Hq, Sq), q.device, "lse")
+    if probe is not None and (probe.dtype != torch.int32 or not probe.is_contiguous()
+                              or probe.numel() < 4 * grid_size(B, Hq, Sq, d)
+                              or probe.device != q.device):
+        raise ValueError("probe must be a contiguous int32 GPU tensor with >= 4*N elements")
+    _check(lib().attn_fwd_persistent_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                             o.data_ptr(),
+                                             None if lse is None else lse.data_ptr(),
+                                             None if probe is None else probe.data_ptr(),
+                                             B, Hq, Hkv, Sq, Skv, d, int(bool(causal)), scale,
+                                             int(mapping)),
+           "attn_fwd_persistent_noalloc")
     return o
 
 

@@ -111,9 +111,12 @@ int env_num_xcd() {
     return (int)v;
 }
 
+// queue: the persistent form's caller-owned tile queues, or NULL; with
+// use_static_queue the persistent form runs on the library's own queue array,
+// cleared by a kernel on the stream right before the launch.
 int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv, int Sq,
         int Skv, int d, int causal, float scale, int mapping, int32_t *probe, float *lse,
-        int32_t *queue = nullptr) {
+        int32_t *queue = nullptr, bool use_static_queue = false) {
     int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
     if (rc) return rc;
     if (lse) {
@@ -145,13 +148,21 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.order = order_bits(mapping);
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
     int grid = B * Hq * a.NB;
-    if (queue) {   // persistent form: one workgroup per compute unit, or per tile if fewer
+    if (queue || use_static_queue) {   // persistent form: one workgroup per compute unit, or per tile if fewer
         const int ncu = num_cu();
         if (ncu < 0) return ncu;
         if (nx > attn::kQueueMaxXcd) return ATTN_ERR_UNSUPPORTED;
         // With more workgroups than tiles the idle ones would take other XCDs'
         // tiles before those XCDs' own workgroups start.
         grid = grid < ncu ? grid : ncu;
+    }
+    if (use_static_queue) {
+        int *sq = nullptr;
+        hipError_t e = attn::static_queue(&sq);
+        if (e != hipSuccess) return hip_fail(e);
+        e = attn::launch_clear_queue(sq, t_stream);
+        if (e != hipSuccess) return hip_fail(e);
+        a.queue = sq;
     }
     hipError_t e = attn::launch_attn_fwd(a, d, causal != 0, mapping & 0xf, grid, t_stream);
     if (e != hipSuccess) return hip_fail(e);
@@ -243,6 +254,15 @@ int attn_fwd_persistent(const void *q, const void *k, const void *v, void *o, fl
         (lse && overlaps(queue, qb, lse, (int64_t)B * Hq * Sq * 4)))
         return ATTN_ERR_ALIAS;
     return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe, lse, queue);
+}
+
+int attn_fwd_persistent_noalloc(const void *q, const void *k, const void *v, void *o, float *lse,
+                                int32_t *probe, int B, int Hq, int Hkv, int Sq, int Skv, int d,
+                                int causal, float scale, int mapping) {
+    if (((uintptr_t)probe & 3u)) return ATTN_ERR_ALIGN;
+    if (d != 128) return ATTN_ERR_UNSUPPORTED;
+    return run(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, causal, scale, mapping, probe, lse, nullptr,
+               true);
 }
 
 int attn_fwd_probe(const void *q, const void *k, const void *v, void *o, int B, int Hq, int Hkv,

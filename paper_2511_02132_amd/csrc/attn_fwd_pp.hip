@@ -31,6 +31,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "attn_device.h"
 #include "attn_internal.h"
 #include "attn_numa.h"
@@ -612,7 +614,45 @@ hipError_t launch_pp_mapping(const KernelArgs &a, int mapping, int grid, hipStre
     }
 }
 
+// The tile queues of attn_fwd_persistent_noalloc: a device array the library
+// owns, for callers that cannot allocate device memory.  Every GPU holds its
+// own copy (zero when the code object loads) until the process ends.  In host
+// code `scratch` names a host-side stand-in, not the device address: the
+// address comes from hipGetSymbolAddress, once per device (static_queue).
+static __device__ __align__(256) int scratch[kQueueInts];
+
+// Zeroes a queue buffer on the stream before a launch that uses it (a kernel,
+// not hipMemsetAsync, so that the launch sequence can be captured in a graph).
+__global__ __launch_bounds__(64, 1) void clear_queue_kernel(int *queue) {
+    if (threadIdx.x < kQueueInts) queue[threadIdx.x] = 0;
+}
+
 }  // namespace
+
+hipError_t static_queue(int **queue) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static int *ptrs[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (ptrs[dev] == nullptr) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        ptrs[dev] = (int *)p;
+    }
+    *queue = ptrs[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_clear_queue(int *queue, hipStream_t stream) {
+    hipLaunchKernelGGL(clear_queue_kernel, dim3(1), dim3(64), 0, stream, queue);
+    return hipGetLastError();
+}
 
 hipError_t launch_attn_fwd_d128(const KernelArgs &a, bool causal, int mapping, int grid,
                                 hipStream_t stream) {

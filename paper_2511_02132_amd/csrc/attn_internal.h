@@ -171,6 +171,11 @@ hipError_t launch_attn_fwd(const KernelArgs &args, int d, bool causal, int mappi
 // The head-dimension-128 kernel (attn_fwd_pp.hip).
 hipError_t launch_attn_fwd_d128(const KernelArgs &args, bool causal, int mapping, int grid,
                                 hipStream_t stream);
+// Device address of the library-owned tile-queue array (kQueueInts int32) on
+// the current device, looked up once per device (attn_fwd_pp.hip).
+hipError_t static_queue(int **queue);
+// Enqueue a one-workgroup kernel that zeroes kQueueInts int32 at `queue`.
+hipError_t launch_clear_queue(int *queue, hipStream_t stream);
 // The backward pass (attn_bwd.hip): D, then dK/dV, then dQ, on one stream.
 hipError_t launch_attn_bwd(const BwdArgs &args, bool causal, int mapping, hipStream_t stream);
 // The dQ kernel alone (attn_bwd_dq.hip); launch_attn_bwd calls it last.

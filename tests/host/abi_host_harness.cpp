@@ -25,7 +25,7 @@
 namespace {
 
 bool g_fail_device = false;   // the stub hipGetDevice fails while set
-int g_fwd_launches = 0, g_bwd_launches = 0, g_calib_launches = 0;
+int g_fwd_launches = 0, g_bwd_launches = 0, g_calib_launches = 0, g_clears = 0;
 attn::KernelArgs g_fwd{};
 int g_fwd_d = 0, g_fwd_mapping = -1, g_fwd_grid = 0;
 bool g_fwd_causal = false;
@@ -33,6 +33,8 @@ attn::BwdArgs g_bwd{};
 int g_bwd_mapping = -1;
 bool g_bwd_causal = false;
 int g_calib_grid = 0, g_calib_iters = 0;
+int *g_cleared = nullptr;
+alignas(256) int g_static_queue[attn::kQueueInts];
 
 int g_checks = 0;
 
@@ -92,6 +94,17 @@ hipError_t launch_calib_mfma(int grid, int iters, int64_t *, float *, hipStream_
     ++g_calib_launches;
     g_calib_grid = grid;
     g_calib_iters = iters;
+    return hipSuccess;
+}
+
+hipError_t static_queue(int **queue) {
+    *queue = g_static_queue;
+    return hipSuccess;
+}
+
+hipError_t launch_clear_queue(int *queue, hipStream_t) {
+    ++g_clears;
+    g_cleared = queue;
     return hipSuccess;
 }
 
@@ -252,6 +265,24 @@ void check_persistent() {
     CHECK(pers(queue, nullptr, 1, 4, 4, 512, 128) == ATTN_ERR_UNSUPPORTED);
     unsetenv("ATTN_NUM_XCD");
 
+    // the entry point that allocates nothing: the library's queue, cleared first
+    auto noalloc = [&](int32_t *probe, int B, int Hq, int Hkv, int S, int d, uintptr_t o) {
+        return attn_fwd_persistent_noalloc(P(kQ), P(kK), P(kV), P(o), lse, probe, B, Hq, Hkv, S, S,
+                                           d, 1, 0.088f, 0x12);
+    };
+    const int clears = g_clears, launches = g_fwd_launches;
+    CHECK(noalloc(nullptr, 1, 4, 4, 512, 64, kO) == ATTN_ERR_UNSUPPORTED);
+    CHECK(noalloc((int32_t *)P(kP + 2), 1, 4, 4, 512, 128, kO) == ATTN_ERR_ALIGN);
+    CHECK(noalloc(nullptr, 1, 4, 4, 512, 128, kQ) == ATTN_ERR_ALIAS);
+    CHECK(noalloc(nullptr, 1, 4, 3, 512, 128, kO) == ATTN_ERR_SHAPE);
+    setenv("ATTN_NUM_XCD", "33", 1);
+    CHECK(noalloc(nullptr, 1, 4, 4, 512, 128, kO) == ATTN_ERR_UNSUPPORTED);
+    unsetenv("ATTN_NUM_XCD");
+    CHECK(g_clears == clears && g_fwd_launches == launches);   // rejected before any launch
+    CHECK(noalloc((int32_t *)P(kP), 2, 16, 4, 700, 128, kO) == ATTN_OK);
+    CHECK(g_clears == clears + 1 && g_fwd_launches == launches + 1);
+    CHECK(g_cleared == g_static_queue && g_fwd.queue == g_static_queue);
+    CHECK(g_fwd_grid == 2 * 16 * 3 && g_fwd.probe == (int32_t *)P(kP) && g_fwd.lse == lse);
 }
 
 void check_backward() {

@@ -4,7 +4,8 @@ tests/host/abi_host_harness.cpp is linked with paper_2511_02132_amd/csrc/attn_ab
 (built for the host by g++, no device code) and stubs of the kernel launchers
 and of the HIP runtime calls.  It drives every entry point through its error
 paths and ragged shapes: validation codes, pointer alignment, every
-input/output overlap of the backward, the persistent form's queue checks, the launch arguments each call derives, the
+input/output overlap of the backward, the persistent forms' queue checks (the
+allocation-free one included), the launch arguments each call derives, the
 HIP-failure path, and attn_map_tiles on ragged shapes, whose tables must equal
 the oracle enumeration.  Any out-of-bounds access, leak or undefined behaviour
 aborts the run.
