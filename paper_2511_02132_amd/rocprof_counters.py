@@ -47,6 +47,92 @@ def variant_of(kernel_name: str):
     return MAPPING_NAMES[int(m.group(2))] + order_suffix(int(m.group(3)))
 
 
+# backward kernels: attn_bwd_dkdv_kernel<causal, mapping, order>, attn_bwd_dq_kernel<...>
+BWD_KERNEL_RE = re.compile(r"attn_bwd_(dkdv|dq)_kernel<(true|false), (\d), (\d)>")
+
+
+def kernel_of(kernel_name: str):
+    """Display name of an attention kernel: the forward's variant, 'dK/dV <variant>'
+    or 'dQ <variant>' for the backward's gradient kernels, 'D' for its row-statistics
+    kernel; None for any other kernel."""
+    v = variant_of(kernel_name)
+    if v is not None:
+        return v
+    m = BWD_KERNEL_RE.search(kernel_name)
+    if m:
+        # the dK/dV kernel carries only the block-major bit of the order
+        return ("dK/dV " if m.group(1) == "dkdv" else "dQ ") + \
+            MAPPING_NAMES[int(m.group(3))] + order_suffix(int(m.group(4)))
+    if "attn_bwd_delta_kernel" in kernel_name:
+        return "D"
+    return None
+
+
+def summarise_kernels(dirs):
+    """{kernel display name: {counter: mean per dispatch}} over every dispatch of
+    the passes in dirs, plus the copy-kernel scale factors of FETCH_SIZE and
+    WRITE_SIZE (from a 256 MiB device copy in the run)."""
+    acc = defaultdict(lambda: defaultdict(list))
+    copy = defaultdict(list)
+    for d in dirs:
+        for did, kname, grid, cname, val in read_csv(d):
+            k = kernel_of(kname)
+            if k is not None:
+                acc[k][cname].append(val)
+            elif "copy" in kname.lower():
+                copy[cname].append(val)
+    copy_bytes = 256 * 2 ** 20
+    fac = {c: copy_bytes / (sum(v) / len(v) * 1024) for c, v in copy.items()
+           if c in ("FETCH_SIZE", "WRITE_SIZE") and v}
+    out = {}
+    for k, cs in acc.items():
+        out[k] = {c: sum(v) / len(v) for c, v in cs.items()}
+    return out, fac
+
+
+def write_kernels_md(out: str, title: str, cmd: str, dirs, note: str = ""):
+    """Per-kernel counter table (MFMA utilisation, LDS instructions per MFMA,
+    LDS waits, L2 hits, HBM bytes) of the passes in dirs."""
+    from paper_2511_02132_amd.build import kernel_source_hash
+
+    res, fac = summarise_kernels(dirs)
+    lines = ["# %s" % title, "", "Commands (run from the repository root; `cd /tmp` first, "
+             "paths absolute in the run):", "", "```", cmd.strip(), "```", "",
+             "Values are means per dispatch over the dispatches of each kernel in the run.", ""]
+    if note:
+        lines += [note, ""]
+    if fac:
+        lines.append("Copy-kernel scale factors (256 MiB device copy): %s." % ", ".join(
+            "%s x%.4f" % (c, f) for c, f in sorted(fac.items())))
+    lines += ["Kernel source sha256[:16] (forward kernels): `%s`" % kernel_source_hash(), "",
+              "| kernel | MFMA util % | MFMA instr | LDS instr | LDS / MFMA | LDS wait / LDS instr "
+              "| VALU instr | L2 hit | HBM bytes read | HBM bytes written |",
+              "|---|---|---|---|---|---|---|---|---|---|"]
+
+    def f(v, fmt):
+        return fmt % v if v is not None else "-"
+    for k in sorted(res):
+        e = res[k]
+        mf, lds = e.get("SQ_INSTS_MFMA"), e.get("SQ_INSTS_LDS")
+        hit, miss = e.get("TCC_HIT"), e.get("TCC_MISS")
+        rd = e["FETCH_SIZE"] * 1024 * fac["FETCH_SIZE"] if "FETCH_SIZE" in e and "FETCH_SIZE" in fac \
+            else None
+        wr = e["WRITE_SIZE"] * 1024 * fac["WRITE_SIZE"] if "WRITE_SIZE" in e and "WRITE_SIZE" in fac \
+            else None
+        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s | %s | %s |" % (
+            k, f(e.get("MfmaUtil"), "%.1f"), f(mf, "%.3e"), f(lds, "%.3e"),
+            f(lds / mf if lds is not None and mf else None, "%.2f"),
+            f(e["SQ_WAIT_INST_LDS"] / lds if "SQ_WAIT_INST_LDS" in e and lds else None, "%.2f"),
+            f(e.get("SQ_INSTS_VALU"), "%.3e"),
+            f(100.0 * hit / (hit + miss) if hit is not None and miss is not None and hit + miss > 0
+              else None, "%.1f%%"),
+            f(rd, "%.3e"), f(wr, "%.3e")))
+    data = {"kernel_source_sha256": kernel_source_hash(), "scale": fac, "per_kernel": res}
+    lines += ["", "```json", json.dumps(data, indent=1, sort_keys=True), "```", ""]
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+
+
 def read_csv(d: str):
     """rows of run_counter_collection.csv: (dispatch, kernel, grid, counter, value)."""
     path = os.path.join(d, "run_counter_collection.csv")
@@ -212,18 +298,21 @@ def write_md(out: str, workload: str, cmd: str, result, fetch_fac, write_fac, xc
     lines += ["L2 read hit: bounds on the hit rate of read requests alone, from TCC_HIT, "
               "TCC_READ and TCC_WRITE (between no write hitting and every write hitting).", ""]
     lines += ["", "| variant | L2 hit | L2 read hit | L2 hit per XCD (min..max) | HBM bytes / launch | "
-                  "/ compulsory | MFMA util % | LDS bank-conflict cycles |",
-              "|---|---|---|---|---|---|---|---|"]
+                  "/ compulsory | MFMA util % | LDS instr / MFMA | LDS bank-conflict cycles |",
+              "|---|---|---|---|---|---|---|---|---|"]
     for v, e in result.items():
         px = e.get("l2_hit_rate_per_xcd")
         hb = e.get("hbm_bytes_per_launch")
         rb = e.get("l2_read_hit_rate_bounds")
-        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s |" % (
+        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s | %s |" % (
             v, "%.1f%%" % (100 * e["l2_hit_rate"]) if "l2_hit_rate" in e else "-",
             "%.1f..%.1f%%" % (100 * rb[0], 100 * rb[1]) if rb else "-",
             "%.1f..%.1f%%" % (100 * min(px), 100 * max(px)) if px else "-",
             "%.3e" % hb if hb else "-", "%.2f" % (hb / comp) if hb else "-",
-            e.get("mfma_util_pct", "-"), "%.3e" % e["sq_lds_bank_conflict"]
+            e.get("mfma_util_pct", "-"),
+            "%.2f" % (e["sq_insts_lds"] / e["sq_insts_mfma"])
+            if e.get("sq_insts_mfma") and "sq_insts_lds" in e else "-",
+            "%.3e" % e["sq_lds_bank_conflict"]
             if "sq_lds_bank_conflict" in e else "-"))
     data = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
             "compulsory_bytes": comp, "fetch_scale": fetch_fac, "write_scale": write_fac,
@@ -273,9 +362,15 @@ def main(argv=None):
     p.add_argument("--cmd", default="", help="the commands that produced the passes")
     p.add_argument("--stats-csv", help="kernel_stats.csv of a --kernel-trace --stats run")
     p.add_argument("--bench-json", help="the bench.py output of that run")
+    p.add_argument("--per-kernel", metavar="TITLE",
+                   help="write a per-kernel counter table (any attention kernels, the "
+                        "backward's included) with this title")
+    p.add_argument("--note", default="")
     p.add_argument("dirs", nargs="*")
     a = p.parse_args(argv)
-    if a.stats_csv:
+    if a.per_kernel:
+        write_kernels_md(a.out, a.per_kernel, a.cmd, a.dirs, a.note)
+    elif a.stats_csv:
         write_stats_md(a.out, a.stats_csv, a.bench_json, a.cmd)
     else:
         res = summarise(a.dirs, a.workload)

@@ -33,6 +33,7 @@ from __future__ import annotations
 import argparse
 import csv
 import json
+import math
 import os
 import re
 import statistics
@@ -81,7 +82,12 @@ def parse(argv=None):
     p.add_argument("--non-causal", action="store_true")
     p.add_argument("--d", type=int, default=D, choices=(56, 64, 128), help="head dimension")
     p.add_argument("--pass", dest="which", choices=("fwd", "bwd"), default="fwd")
-    p.add_argument("--reps", type=int, default=2)
+    p.add_argument("--reps", type=int, default=5,
+                   help="interleaved timed launches per variant, at least")
+    p.add_argument("--min-timed-ms", type=float, default=1500.0,
+                   help="more reps (up to --max-reps) until each variant has about this much "
+                        "timed launch time")
+    p.add_argument("--max-reps", type=int, default=20)
     p.add_argument("--warmup-ms", type=float, default=1000.0,
                    help="untimed launches for this long before the first configuration: the "
                         "shader clock of a process's first few hundred milliseconds runs low")
@@ -98,6 +104,32 @@ def parse(argv=None):
     if a.heads is None:
         a.heads = list(MHA_HEADS if a.family == "mha" else GQA_QHEADS)
     return a
+
+
+def iqr(xs) -> float:
+    """Interquartile range (linear interpolation between order statistics)."""
+    ys = sorted(xs)
+
+    def q(p):
+        x = p * (len(ys) - 1)
+        i = int(math.floor(x))
+        j = min(i + 1, len(ys) - 1)
+        return ys[i] + (ys[j] - ys[i]) * (x - i)
+    return q(0.75) - q(0.25)
+
+
+def compare(r, x, y):
+    """+1 if variant x is faster than y in record r by more than the spread of
+    either (the larger interquartile range of the two launch times), -1 if
+    slower by more than that, 0 otherwise (within the spread).  Records
+    without spreads compare medians."""
+    mx, my = r["ms"][x], r["ms"][y]
+    spread = max(r.get("ms_iqr", {}).get(x, 0.0), r.get("ms_iqr", {}).get(y, 0.0))
+    if my - mx > spread:
+        return 1
+    if mx - my > spread:
+        return -1
+    return 0
 
 
 def run(a):
@@ -146,7 +178,19 @@ def run(a):
                 torch.cuda.synchronize()
                 if time.perf_counter() >= t_end:
                     break
-        for _ in range(reps):
+        if not a.profile:
+            # reps from the duration of one launch: short configurations get more
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch(vs[0][1])
+            e1.record(stream)
+            torch.cuda.synchronize()
+            est = max(e0.elapsed_time(e1), 1e-3)
+            reps = min(max(a.reps, int(math.ceil(a.min_timed_ms / est))), max(a.max_reps, a.reps))
+        for rep in range(reps):
+            if not a.profile and est * len(vs) > 5000:
+                print("  %s rep %d/%d" % (json.dumps(c), rep + 1, reps), file=sys.stderr, flush=True)
             for name, m in vs:
                 flush.zero_()
                 e0 = torch.cuda.Event(enable_timing=True)
@@ -160,7 +204,10 @@ def run(a):
                 times[name].append(e0.elapsed_time(e1))
         f = flops(c, causal, a.d) * (2.5 if a.which == "bwd" else 1.0)
         rec = {"family": a.family, "pass": a.which, "causal": causal, **c, "d": a.d,
+               "reps": reps,
                "ms": {n: round(statistics.median(t), 4) for n, t in times.items()},
+               "ms_min": {n: round(min(t), 4) for n, t in times.items()},
+               "ms_iqr": {n: round(iqr(t), 4) for n, t in times.items()},
                "tflops": {n: round(f / statistics.median(t) / 1e9, 1) for n, t in times.items()}}
         line = json.dumps(rec)
         print(line, flush=True)
@@ -171,6 +218,13 @@ def run(a):
         if a.which == "bwd":
             del do, lse, grads
         torch.cuda.empty_cache()
+    if a.profile:
+        # a plain copy of known size (256 MiB, twice): scales FETCH_SIZE / WRITE_SIZE to bytes
+        src = torch.ones(256 * 2 ** 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
     if a.profile and a.manifest:
         with open(a.manifest, "w") as fm:
             json.dump(manifest, fm)
@@ -263,6 +317,55 @@ def l2_counters_by_launch(counters_dir: str, manifest_path: str):
     return out
 
 
+def comparisons(recs, names, sh, causal):
+    """Win / tie / loss counts of the paper's mapping against block-first, a
+    win counting only when the gap exceeds the larger interquartile range of
+    the two variants' launch times (compare)."""
+    if not recs:
+        return []
+    spreads = "ms_iqr" in recs[0]
+    out = ["", "Comparisons per configuration (%s):" % (
+        "a win or a loss only where the gap of the medians exceeds the larger interquartile "
+        "range of the two variants' launch times; otherwise a tie" if spreads else
+        "medians only: these records carry no spread"), ""]
+    pairs = [("swizzled_head_first", "naive_block_first", "same (increasing) block order")]
+    if causal:
+        pairs.append(("swizzled_head_first+heavy_first", "naive_block_first+heavy_first",
+                      "same (heavy-first) block order"))
+    best_bf = [n for n in ("naive_block_first", "swizzled_block_first") + (
+        ("naive_block_first+heavy_first", "swizzled_block_first+heavy_first") if causal else ())
+        if n in names]
+    heads = [n for n in ("swizzled_head_first+heavy_first" if causal else "swizzled_head_first",
+                         "swizzled_head_first+heavy_first+xcd_block_major" if causal else
+                         "swizzled_head_first+xcd_block_major") if n in names]
+    out += ["| comparison | wins | ties | losses | losses (ratio of medians) |", "|---|---|---|---|---|"]
+
+    def row(label, res):
+        w = sum(1 for x in res if x[0] > 0)
+        t = sum(1 for x in res if x[0] == 0)
+        lo = [x for x in res if x[0] < 0]
+        det = ", ".join("%dK B%d H%d/%d %.3f" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"], q)
+                        for _, r, q in lo) or "-"
+        out.append("| %s | %d | %d | %d | %s |" % (label, w, t, len(lo), det))
+
+    for x, y, how in pairs:
+        if x in names and y in names:
+            row("%s vs %s (%s)" % (sh(x), sh(y), how),
+                [(compare(r, x, y), r, r["ms"][y] / r["ms"][x]) for r in recs])
+    for x in heads:
+        res = []
+        for r in recs:
+            y = min(best_bf, key=lambda n: r["ms"][n])
+            res.append((compare(r, x, y), r, r["ms"][y] / r["ms"][x]))
+        row("%s vs the fastest block-first order of each configuration (%s)" % (
+            sh(x), ", ".join(sh(n) for n in best_bf)), res)
+    if spreads:
+        worst = max(max(r["ms_iqr"][n] / r["ms"][n] for n in names) for r in recs)
+        out += ["", "Largest interquartile range of a variant's launch times: %.1f%% of its "
+                "median." % (100 * worst)]
+    return out
+
+
 def summarise(a):
     recs = {}
     for path in a.timing:   # a later file's record of a configuration replaces an earlier one
@@ -297,7 +400,8 @@ def summarise(a):
         lines += ["TFLOP/s of the gradient kernels (D, dK/dV, dQ) in the FlashAttention "
                   "convention: 2.5x the forward's 4*B*Hq*S*S*d (halved when causal).", ""]
     lines += ["Each cell: TFLOP/s (median of the interleaved, L2+MALL-flushed launches), then "
-              "relative to %s." % base]
+              "relative to %s.  reps: timed launches per variant; max IQR: the largest "
+              "interquartile range of a variant's launch times, relative to its median." % base]
     if l2:
         lines += ["Second table: L2 hit rate of one launch per variant (rocprofv3 TCC_HIT / "
                   "(TCC_HIT + TCC_MISS))."]
@@ -312,10 +416,15 @@ def summarise(a):
     if a.cmd:
         lines += ["Commands:", "", "```", a.cmd, "```", ""]
     hdr = "| S | B | Hq/Hkv | " + " | ".join(sh(n) for n in names) + " |"
-    lines += [hdr, "|" + "---|" * (3 + len(names))]
+    reps_col = bool(recs) and "reps" in recs[0]
+    lines += [hdr[:-1] + ("| reps | max IQR |" if reps_col else "|"),
+              "|" + "---|" * (3 + len(names) + (2 if reps_col else 0))]
     for r in recs:
         ref = r["tflops"][base]
         cells = ["%.0f (%.2f)" % (r["tflops"][n], r["tflops"][n] / ref) for n in names]
+        if reps_col:
+            cells += [str(r["reps"]), "%.1f%%" % (100 * max(r["ms_iqr"][n] / r["ms"][n]
+                                                            for n in names))]
         lines.append("| %dK | %d | %d/%d | %s |" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"],
                                                    " | ".join(cells)))
     if l2:
@@ -337,12 +446,11 @@ def summarise(a):
             lines.append("| %dK | %d | %d/%d | %s |" % (r["S"] // 1024, r["B"], r["Hq"], r["Hkv"],
                                                        " | ".join(cells)))
     # geometric-mean speed relative to the method, per variant
-    import math
-
     lines += ["", "Geometric mean over the configurations, relative to %s:" % base, ""]
     for n in names:
         g = math.exp(sum(math.log(r["tflops"][n] / r["tflops"][base]) for r in recs) / len(recs))
         lines.append("- %s: %.3f" % (n, g))
+    lines += comparisons(recs, names, sh, causal)
     text = "\n".join(lines) + "\n"
     if a.out:
         with open(a.out, "w") as f:

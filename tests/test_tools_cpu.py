@@ -226,3 +226,60 @@ def test_sweep_kv_heads_option():
     assert sweep.parse([]).warmup_ms == 1000.0
     # the mha family ignores it: every q-head has its own KV head
     assert [c["Hkv"] for c in sweep.configs("mha", [4096], [1], [16], 1)] == [16]
+
+
+def test_sweep_spread_comparisons():
+    """A win counts only when the gap of the medians exceeds the larger
+    interquartile range of the two variants' launch times."""
+    assert sweep.iqr([1.0, 2.0, 3.0, 4.0, 5.0]) == 2.0
+    assert sweep.iqr([7.0]) == 0.0
+    r = {"ms": {"a": 1.00, "b": 1.05, "c": 1.01}, "ms_iqr": {"a": 0.02, "b": 0.01, "c": 0.03}}
+    assert sweep.compare(r, "a", "b") == 1 and sweep.compare(r, "b", "a") == -1
+    assert sweep.compare(r, "a", "c") == 0 and sweep.compare(r, "c", "a") == 0
+    assert sweep.compare({"ms": {"a": 1.0, "b": 1.001}}, "a", "b") == 1   # no spreads: medians
+
+    names = [n for n, _ in pa.variants(True)]
+    recs = []
+    for i, slow in enumerate((1.10, 1.001, 0.95)):
+        ms = {n: 1.0 for n in names}
+        ms["naive_block_first+heavy_first"] = slow          # vs the headline: win, tie, loss
+        ms["swizzled_block_first+heavy_first"] = 1.2
+        ms["naive_block_first"] = ms["swizzled_block_first"] = 1.3
+        recs.append({"S": 8192 * (i + 1), "B": 1, "Hq": 32, "Hkv": 32, "ms": ms,
+                     "ms_iqr": {n: 0.01 for n in names}})
+    lines = sweep.comparisons(recs, names, lambda n: n, True)
+    row = [l for l in lines if l.startswith("| swizzled_head_first+heavy_first vs the fastest")][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[1:4] == ["1", "1", "1"], cells
+    assert "24K B1 H32/32" in cells[4]
+
+
+def test_per_kernel_counter_table(tmp_path):
+    """Backward kernels are named by kind and variant; the per-kernel table
+    averages each counter over a kernel's dispatches, scales FETCH_SIZE and
+    WRITE_SIZE by the copy kernel, and reports LDS instructions per MFMA."""
+    assert rc.kernel_of("void attn::(anonymous namespace)::attn_bwd_dkdv_kernel<true, 2, 2>"
+                        "(attn::BwdArgs)") == "dK/dV swizzled_head_first+xcd_block_major"
+    assert rc.kernel_of("void attn::(anonymous namespace)::attn_bwd_dq_kernel<false, 0, 1>"
+                        "(attn::BwdArgs)") == "dQ naive_block_first+heavy_first"
+    assert rc.kernel_of("attn::(anonymous namespace)::attn_bwd_delta_kernel(attn::BwdArgs)") == "D"
+    assert rc.kernel_of("void at::native::elementwise_kernel<...>") is None
+    d = tmp_path / "pass"
+    d.mkdir()
+    dq = "void attn::(anonymous namespace)::attn_bwd_dq_kernel<true, 2, 1>(attn::BwdArgs)"
+    rows = [(1, dq, 256, "SQ_INSTS_MFMA", 100.0), (1, dq, 256, "SQ_INSTS_LDS", 150.0),
+            (2, dq, 256, "SQ_INSTS_MFMA", 300.0), (2, dq, 256, "SQ_INSTS_LDS", 450.0),
+            (1, dq, 256, "FETCH_SIZE", 10.0), (3, "__amd_rocclr_copyBuffer", 256, "FETCH_SIZE",
+                                                131072.0)]
+    with open(d / "run_counter_collection.csv", "w") as f:
+        f.write("Dispatch_Id,Kernel_Name,Grid_Size,Counter_Name,Counter_Value\n")
+        for r in rows:
+            f.write('%d,"%s",%d,%s,%f\n' % r)
+    res, fac = rc.summarise_kernels([str(d)])
+    e = res["dQ swizzled_head_first+heavy_first"]
+    assert e["SQ_INSTS_MFMA"] == 200.0 and e["SQ_INSTS_LDS"] == 300.0
+    assert abs(fac["FETCH_SIZE"] - 2.0) < 1e-12
+    out = tmp_path / "k.md"
+    rc.write_kernels_md(str(out), "T", "CMD", [str(d)])
+    line = [l for l in out.read_text().splitlines() if l.startswith("| dQ ")][0]
+    assert "| 1.50 |" in line and "2.048e+04" in line
