@@ -61,10 +61,10 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
-def variants(causal: bool):
+def variants(causal: bool, d: int):
     """(name, mapping value) pairs measured per mapping."""
     import paper_2511_02132_amd as pa
-    return pa.variants(causal)
+    return pa.variants(causal, d)
 
 
 def kernel_source_hash() -> str:
@@ -136,7 +136,7 @@ def main():
 
     if args.profile:
         # Each (mapping, order) is its own kernel symbol, so one run covers all.
-        for _, m in variants(causal):
+        for _, m in variants(causal, d):
             for _ in range(args.profile_launches):
                 step(m)
         # One workgroup (wid 0 runs on XCD 0): shows which counter instances belong to XCD 0.
@@ -149,7 +149,7 @@ def main():
         for _ in range(args.profile_launches):
             dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"profile": args.workload, "variants": [n for n, _ in variants(causal)],
+        print(json.dumps({"profile": args.workload, "variants": [n for n, _ in variants(causal, d)],
                           "copy_bytes_each_way": src.numel()}), flush=True)
         return
 
@@ -196,7 +196,7 @@ def main():
 
     # ---- per mapping: interleaved, cold (L2 + MALL flushed) and warm
     flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device=dev)
-    vs = variants(causal)
+    vs = variants(causal, d)
     cold, warm = timed_variants(torch, stream, flush, step, vs, args.reps, warm_too=True)
     counters = counter_summary(args.workload)
     per_mapping = {}
@@ -305,7 +305,7 @@ def small_workload(args, torch, dev, stream, flush, ai, pa):
     def st(m):
         pa.attn_fwd(qs, ks, vs_, os_, causal=w["causal"], scale=sc, mapping=m, stream=stream)
 
-    vs = variants(w["causal"])
+    vs = variants(w["causal"], w["d"])
     for _, m in vs:   # one untimed launch each
         st(m)
     torch.cuda.synchronize()

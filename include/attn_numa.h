@@ -65,7 +65,22 @@ enum {
      * row blocks (the imbalance shrinks like 1/blocks, and at long contexts
      * head-major order shares K/V better); otherwise the order is unchanged.
      * Not part of the paper's mappings. */
-    ATTN_ORDER_XCD_BLOCK_MAJOR = 0x20
+    ATTN_ORDER_XCD_BLOCK_MAJOR = 0x20,
+    /* Optional flag for the dispatched forward with head dimension 128
+     * (attn_fwd, attn_fwd_lse, attn_fwd_probe; ATTN_ERR_UNSUPPORTED for
+     * another d or a persistent form, ATTN_ERR_MAPPING for attn_bwd): the grid
+     * has P = ceil(NB/2) slots per head instead of NB row blocks (NB =
+     * ceil(Sq/attn_block_m(d))).  The mapping and the other flags place the
+     * B*Hq*P slots exactly as they place tiles, with P in place of NB, and
+     * the workgroup of slot p computes row block NB-1-p and then row block p
+     * (once, if they coincide).  Under a causal mask with Sq == Skv block m
+     * costs m+1 block-widths of K/V, so every pair costs NB+1 (the middle
+     * block of an odd NB about half): the workgroups an XCD hands to its four
+     * shader engines cost the same whatever their order, and each XCD still
+     * serves the contiguous slots of one (batch, head) at a time under
+     * ATTN_MAP_SWIZZLED_HEAD_FIRST.  The output is bitwise that of the order
+     * without the flag.  Not part of the paper's mappings. */
+    ATTN_ORDER_PAIRED = 0x40
 };
 
 enum {
@@ -73,7 +88,7 @@ enum {
     ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
     ATTN_ERR_SHAPE = -2,       /* a dimension <= 0, Hq % Hkv != 0, or a size limit exceeded */
     ATTN_ERR_UNSUPPORTED = -3, /* head dimension other than 56, 64 or 128 (or a form that lacks it) */
-    ATTN_ERR_MAPPING = -4,     /* mapping not one of ATTN_MAP_* */
+    ATTN_ERR_MAPPING = -4,     /* mapping not one of ATTN_MAP_* with the flags allowed for it */
     ATTN_ERR_SCALE = -5,       /* scale not finite or not > 0 */
     ATTN_ERR_ALIGN = -6,       /* a bf16 tensor not 16-byte aligned, or an fp32/int32 buffer not 4-byte aligned */
     ATTN_ERR_HIP = -7,         /* a HIP runtime call failed; see attn_last_hip_error() */
@@ -102,8 +117,9 @@ enum {
  *     with bf16 inputs, fp32 accumulation and bf16 rounding (RNE) of P and O.
  * mapping : one of ATTN_MAP_NAIVE_BLOCK_FIRST, ATTN_MAP_NAIVE_HEAD_FIRST,
  *     ATTN_MAP_SWIZZLED_HEAD_FIRST, ATTN_MAP_SWIZZLED_BLOCK_FIRST, optionally
- *     | ATTN_ORDER_HEAVY_FIRST, and for ATTN_MAP_SWIZZLED_HEAD_FIRST optionally
- *     | ATTN_ORDER_XCD_BLOCK_MAJOR.
+ *     | ATTN_ORDER_HEAVY_FIRST, for ATTN_MAP_SWIZZLED_HEAD_FIRST optionally
+ *     | ATTN_ORDER_XCD_BLOCK_MAJOR, and for d = 128 optionally
+ *     | ATTN_ORDER_PAIRED.
  *
  * Ownership: all buffers belong to the caller; nothing is retained after the
  * call returns and nothing is allocated.  The kernel is enqueued on the stream
@@ -119,6 +135,9 @@ int attn_fwd(const void *q, const void *k, const void *v, void *o,
  * 3.2, 3.3): the same kernel writes, for every workgroup id wid, four int32
  * values probe[4*wid + 0..3] = (b, hq, m, xcc) where (b, hq, m) is the tile
  * that WG computed and xcc the XCD it ran on (hardware register XCC_ID).
+ * With ATTN_ORDER_PAIRED only the B*Hq*ceil(NB/2) workgroups of the paired
+ * grid write, and m is the first row block of the slot (NB-1-p); the records
+ * past them are left as they were.
  * probe : device pointer to attn_grid_size(B, Hq, Sq, d) * 4 int32, owned by
  * the caller.  Other arguments and behaviour as attn_fwd.
  */
@@ -162,7 +181,8 @@ int attn_fwd_lse(const void *q, const void *k, const void *v, void *o, float *ls
  * dq : output, bf16 [B][Hq][Sq][d].   dk, dv : outputs, bf16 [B][Hkv][Skv][d].
  *     Every element of dq, dk and dv is written.
  * d : 128 only (ATTN_ERR_UNSUPPORTED otherwise).
- * mapping : as attn_fwd.  The dQ kernel decodes its workgroups over
+ * mapping : as attn_fwd, without ATTN_ORDER_PAIRED (ATTN_ERR_MAPPING).  The
+ *     dQ kernel decodes its workgroups over
  *     (b, hq, row block of 128) and the dK/dV kernel over (b, K/V head, key
  *     block of 128) with that mapping; ATTN_ORDER_HEAVY_FIRST reverses the row
  *     blocks of the dQ kernel (the dK/dV kernel's natural order already starts
@@ -199,8 +219,9 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
  * lse : NULL, or as attn_fwd_lse.
  * probe : NULL, or as attn_fwd_probe (indexed by wid; xcc is the XCD that ran
  *     the tile).
- * Other arguments and behaviour as attn_fwd; ATTN_ERR_UNSUPPORTED for d != 128
- * or more than 32 XCDs.  The output is bitwise that of attn_fwd.
+ * Other arguments and behaviour as attn_fwd; ATTN_ERR_UNSUPPORTED for d != 128,
+ * more than 32 XCDs, or ATTN_ORDER_PAIRED (the queues already balance the
+ * work).  The output is bitwise that of attn_fwd.
  */
 #define ATTN_QUEUE_INTS 64
 int attn_fwd_persistent(const void *q, const void *k, const void *v, void *o, float *lse,
@@ -226,9 +247,9 @@ int attn_fwd_persistent(const void *q, const void *k, const void *v, void *o, fl
  * overlap on one GPU (different streams without ordering between them) race
  * on it and may compute tiles twice or not at all; order them on one stream.
  *
- * Errors: as attn_fwd_persistent; ATTN_ERR_UNSUPPORTED for d != 128 or more
- * than 32 XCDs (the array's maximum); ATTN_ERR_HIP if the array's address
- * cannot be obtained.  The output is bitwise that of attn_fwd_persistent.
+ * Errors: as attn_fwd_persistent; ATTN_ERR_UNSUPPORTED for d != 128,
+ * ATTN_ORDER_PAIRED or more than 32 XCDs (the array's maximum); ATTN_ERR_HIP
+ * if the array's address cannot be obtained.  The output is bitwise that of attn_fwd_persistent.
  */
 int attn_fwd_persistent_noalloc(const void *q, const void *k, const void *v, void *o, float *lse,
                                 int32_t *probe, int B, int Hq, int Hkv, int Sq, int Skv,
@@ -243,6 +264,10 @@ int64_t attn_grid_size(int B, int Hq, int Sq, int d);
  * same integer code the kernel prologue runs (Sections 3.2 and 3.3): for
  * wid = 0 .. N-1, N = B*Hq*ceil(Sq/attn_block_m(d)), writes
  * out[3*wid + 0..2] = (b, hq, m) of workgroup wid under `mapping` with NX XCDs.
+ * With ATTN_ORDER_PAIRED (d = 128 only, else ATTN_ERR_UNSUPPORTED) the rows
+ * wid < B*Hq*ceil(NB/2) hold the first row block m = NB-1-p of the
+ * workgroup's slot p (the second is NB-1-m when it differs from m), and the
+ * rows past them hold -1.
  * out : host pointer to N*3 int32, owned by the caller.  No HIP call is made.
  */
 int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *out);

@@ -66,6 +66,15 @@ Order options (not among the paper's mappings):
     applies only when NB <= BLOCK_MAJOR_MAX_BLOCKS = 64: the engine imbalance
     of head-major order shrinks like 1/NB, and at long contexts the K/V
     streams in flight cost more than it saves (measured).
+  * ``paired`` (head dimension 128, forward): the grid has P = ceil(NB/2)
+    slots per head instead of NB row blocks.  The mapping and the options
+    above place the B*Hq*P slots as they would place tiles with P row blocks
+    per head, and the WG of slot p computes row block NB-1-p, then row block p
+    (once when the two coincide, the middle block of an odd NB).  Under a
+    causal mask with Sq == Skv block m costs m+1 block-widths of K/V, so every
+    slot costs NB+1 except that middle one, whatever order the WGs start in.
+    A table entry is the slot's first row block NB-1-p; ``slot_blocks`` lists
+    both.
 """
 
 from __future__ import annotations
@@ -121,10 +130,26 @@ def xcd_piece(x: int, N: int, NX: int) -> tuple:
     return x * q + min(x, r), q + (1 if x < r else 0)
 
 
+def pair_slots(NB: int) -> int:
+    """Slots per head of the paired order: ceil(NB / 2)."""
+    return (NB + 1) // 2
+
+
+def slot_blocks(m_first: int, NB: int) -> list:
+    """Row blocks a paired slot computes, in order, from its first block."""
+    second = NB - 1 - m_first
+    return [m_first] if second == m_first else [m_first, second]
+
+
 def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
             heavy_first: bool = False, xcd_block_major: bool = False,
-            short_head_groups: bool = False) -> tuple:
-    """(b, hq, m) that WG ``wid`` computes under ``mapping``."""
+            short_head_groups: bool = False, paired: bool = False) -> tuple:
+    """(b, hq, m) that WG ``wid`` computes under ``mapping`` (with ``paired``,
+    m is the first row block of its slot)."""
+    if paired:
+        b, hq, p = map_wid(mapping, wid, B, Hq, pair_slots(NB), NX, heavy_first,
+                           xcd_block_major, short_head_groups)
+        return b, hq, NB - 1 - p
     N = B * Hq * NB
     if not 0 <= wid < N:
         raise ValueError("wid out of range")
@@ -159,21 +184,22 @@ def map_wid(mapping: int, wid: int, B: int, Hq: int, NB: int, NX: int,
 
 def enumerate_mapping(mapping: int, B: int, Hq: int, Sq: int, BM: int, NX: int,
                       heavy_first: bool = False, xcd_block_major: bool = False,
-                      short_head_groups: bool = False) -> np.ndarray:
-    """Array [N, 3] of (b, hq, m) for wid = 0 .. N-1 (pure-Python loop)."""
+                      short_head_groups: bool = False, paired: bool = False) -> np.ndarray:
+    """Array [N, 3] of (b, hq, m) for wid = 0 .. N-1 (pure-Python loop); with
+    ``paired``, N = B*Hq*ceil(NB/2) and m is each slot's first row block."""
     NB = num_row_blocks(Sq, BM)
-    N = B * Hq * NB
+    N = B * Hq * (pair_slots(NB) if paired else NB)
     out = np.empty((N, 3), dtype=np.int64)
     for wid in range(N):
         out[wid] = map_wid(mapping, wid, B, Hq, NB, NX, heavy_first, xcd_block_major,
-                           short_head_groups)
+                           short_head_groups, paired)
     return out
 
 
 def split_flags(mapping_with_flags: int) -> tuple:
-    """(base mapping, heavy_first, xcd_block_major) of an ABI mapping value."""
+    """(base mapping, heavy_first, xcd_block_major, paired) of an ABI mapping value."""
     return (mapping_with_flags & 0xF, bool(mapping_with_flags & 0x10),
-            bool(mapping_with_flags & 0x20))
+            bool(mapping_with_flags & 0x20), bool(mapping_with_flags & 0x40))
 
 
 def acc_id(b: int, hq: int, Hq: int, Hkv: int) -> int:

@@ -32,6 +32,10 @@ HEAVY_FIRST = 0x10
 # within groups of four heads (heads of at most 64 row blocks; longer ones keep
 # head-major order).
 XCD_BLOCK_MAJOR = 0x20
+# Flag for the dispatched forward with d = 128: one workgroup per pair of row
+# blocks (NB-1-p, then p) of a head, ceil(NB/2) slots per head placed by the
+# mapping; under a causal mask every pair costs the same.
+PAIRED = 0x40
 MAPPINGS = {"naive_block_first": NAIVE_BLOCK_FIRST, "naive_head_first": NAIVE_HEAD_FIRST,
             "swizzled_head_first": SWIZZLED_HEAD_FIRST, "swizzled_block_first": SWIZZLED_BLOCK_FIRST}
 MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
@@ -45,17 +49,25 @@ def variant_name(mapping: int) -> str:
         name += "+heavy_first"
     if mapping & XCD_BLOCK_MAJOR:
         name += "+xcd_block_major"
+    if mapping & PAIRED:
+        name += "+paired"
     return name
 
 
-def variants(causal: bool):
+def variants(causal: bool, d: int = 128, backward: bool = False):
     """(name, mapping value) of every variant the measurements compare: the four
-    mappings; under a causal mask each also with the heavy-first order; and
-    swizzled head-first with the block-major order inside each XCD."""
+    mappings; under a causal mask each also with the heavy-first order;
+    swizzled head-first with the block-major order inside each XCD; and, for the
+    d = 128 forward under a causal mask, the three mappings that keep heads or
+    KV groups together (naive block-first, swizzled head-first, swizzled
+    block-first) with heavy-first paired row blocks."""
     vals = list(range(4)) + [SWIZZLED_HEAD_FIRST | XCD_BLOCK_MAJOR]
     if causal:
         vals = list(range(4)) + [m | HEAVY_FIRST for m in range(4)] + \
             [SWIZZLED_HEAD_FIRST | HEAVY_FIRST | XCD_BLOCK_MAJOR]
+        if d == 128 and not backward:
+            vals += [m | HEAVY_FIRST | PAIRED for m in (NAIVE_BLOCK_FIRST, SWIZZLED_HEAD_FIRST,
+                                                        SWIZZLED_BLOCK_FIRST)]
     return [(variant_name(v), v) for v in vals]
 
 

@@ -71,14 +71,22 @@ bool valid_mapping(int mapping) {
     const int base = mapping & 0xf;
     const int flags = mapping & ~0xf;
     if (base < ATTN_MAP_NAIVE_BLOCK_FIRST || base > ATTN_MAP_SWIZZLED_BLOCK_FIRST) return false;
-    if ((flags & ~(ATTN_ORDER_HEAVY_FIRST | ATTN_ORDER_XCD_BLOCK_MAJOR)) != 0) return false;
+    if ((flags & ~(ATTN_ORDER_HEAVY_FIRST | ATTN_ORDER_XCD_BLOCK_MAJOR | ATTN_ORDER_PAIRED)) != 0)
+        return false;
     // the block-major order inside an XCD's piece is defined for mapping 2 only
     return (flags & ATTN_ORDER_XCD_BLOCK_MAJOR) == 0 || base == ATTN_MAP_SWIZZLED_HEAD_FIRST;
 }
 
 int order_bits(int mapping) {
     return ((mapping & ATTN_ORDER_HEAVY_FIRST) ? attn::kOrderHeavyFirst : 0) |
-           ((mapping & ATTN_ORDER_XCD_BLOCK_MAJOR) ? attn::kOrderXcdBlockMajor : 0);
+           ((mapping & ATTN_ORDER_XCD_BLOCK_MAJOR) ? attn::kOrderXcdBlockMajor : 0) |
+           ((mapping & ATTN_ORDER_PAIRED) ? attn::kOrderPaired : 0);
+}
+
+// Row blocks of a head that one workgroup's grid slot stands for: NB, or the
+// pair slots of the paired order.
+int slots_per_head(int NB, int mapping) {
+    return (mapping & ATTN_ORDER_PAIRED) ? attn::pair_slots(NB) : NB;
 }
 
 bool overlaps(const void *a, int64_t a_bytes, const void *b, int64_t b_bytes) {
@@ -119,6 +127,9 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
         int32_t *queue = nullptr, bool use_static_queue = false) {
     int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
     if (rc) return rc;
+    // pairs exist for the dispatched head-dimension-128 kernel only
+    if ((mapping & ATTN_ORDER_PAIRED) && (d != 128 || queue || use_static_queue))
+        return ATTN_ERR_UNSUPPORTED;
     if (lse) {
         if (((uintptr_t)lse) & 3u) return ATTN_ERR_ALIGN;
         const int64_t lse_bytes = (int64_t)B * Hq * Sq * 4;
@@ -147,7 +158,7 @@ int run(const void *q, const void *k, const void *v, void *o, int B, int Hq, int
     a.NX = nx;
     a.order = order_bits(mapping);
     a.scale_log2 = (float)((double)scale * 1.4426950408889634073599246810019);  // log2(e)
-    int grid = B * Hq * a.NB;
+    int grid = B * Hq * slots_per_head(a.NB, mapping);
     if (queue || use_static_queue) {   // persistent form: one workgroup per compute unit, or per tile if fewer
         const int ncu = num_cu();
         if (ncu < 0) return ncu;
@@ -190,6 +201,7 @@ int attn_bwd(const void *q, const void *k, const void *v, const void *o, const v
     if (!dout || !lse || !delta || !dq || !dk || !dv) return ATTN_ERR_NULL;
     int rc = validate(q, k, v, o, B, Hq, Hkv, Sq, Skv, d, scale, mapping);
     if (rc) return rc;
+    if (mapping & ATTN_ORDER_PAIRED) return ATTN_ERR_MAPPING;   // a forward-only order
     if (d != 128) return ATTN_ERR_UNSUPPORTED;
     if ((((uintptr_t)dout | (uintptr_t)dq | (uintptr_t)dk | (uintptr_t)dv) & 15u) ||
         (((uintptr_t)lse | (uintptr_t)delta) & 3u))
@@ -299,11 +311,19 @@ int attn_map_tiles(int mapping, int B, int Hq, int Sq, int d, int NX, int32_t *o
     if (n < 0) return (int)n;
     if (n > INT32_MAX) return ATTN_ERR_SHAPE;
     const int nb = (Sq + attn::block_m_for(d) - 1) / attn::block_m_for(d);
+    const bool paired = (mapping & ATTN_ORDER_PAIRED) != 0;
+    if (paired && d != 128) return ATTN_ERR_UNSUPPORTED;
     // the four-wave kernel (128-row blocks) uses the 16-head groups for short heads
     const bool short_groups = attn::block_m_for(d) == attn::kBlockM;
+    const int64_t slots = (int64_t)B * Hq * slots_per_head(nb, mapping);
     for (int64_t wid = 0; wid < n; ++wid) {
-        const attn::Tile t = attn::map_wid(mapping & 0xf, order_bits(mapping),
-                                           (int)wid, B, Hq, nb, NX, short_groups);
+        if (wid >= slots) {   // past the paired grid: no workgroup
+            out[3 * wid + 0] = out[3 * wid + 1] = out[3 * wid + 2] = -1;
+            continue;
+        }
+        attn::Tile t = attn::map_wid(mapping & 0xf, order_bits(mapping), (int)wid, B, Hq,
+                                     slots_per_head(nb, mapping), NX, short_groups);
+        if (paired) t.m = nb - 1 - t.m;   // the slot's first row block
         out[3 * wid + 0] = t.b;
         out[3 * wid + 1] = t.hq;
         out[3 * wid + 2] = t.m;
@@ -344,7 +364,7 @@ const char *attn_strerror(int code) {
         case ATTN_ERR_NULL: return "null pointer argument";
         case ATTN_ERR_SHAPE: return "invalid shape (non-positive dimension, Hq % Hkv != 0, or size limit)";
         case ATTN_ERR_UNSUPPORTED: return "unsupported head dimension (forward: 56, 64, 128; backward and persistent forward: 128)";
-        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST, and for 2 | ATTN_ORDER_XCD_BLOCK_MAJOR)";
+        case ATTN_ERR_MAPPING: return "unknown mapping (0 naive block-first, 1 naive head-first, 2 swizzled head-first, 3 swizzled block-first, optionally | ATTN_ORDER_HEAVY_FIRST, for 2 | ATTN_ORDER_XCD_BLOCK_MAJOR, and in the forward | ATTN_ORDER_PAIRED)";
         case ATTN_ERR_SCALE: return "scale must be finite and > 0";
         case ATTN_ERR_ALIGN: return "pointer not aligned (bf16 tensors: 16 bytes; fp32 and int32 buffers: 4 bytes; int64 buffers: 8 bytes)";
         case ATTN_ERR_HIP: return "HIP runtime error";

@@ -118,16 +118,15 @@ __device__ __forceinline__ void wait_copies() {
 // plus the block's Q rows when kQInLds.
 constexpr int kPPLdsBytes = kStages * 2 * kBlockN * 256 + (kQInLds ? kBlockM128 * 256 : 0);
 
-// One tile (b, hq, m) of the output: the whole per-workgroup computation for
-// workgroup id `wid` (decoded by the mapping), with the LDS at `smem`.  It
-// starts and ends with every wave at the same barrier count, so a persistent
-// workgroup can run it repeatedly.
+// One tile (b, hq, m) of the output, with the LDS at `smem`.  It starts and
+// ends with every wave at the same barrier count, so a workgroup can run it
+// repeatedly (a paired slot, the persistent loop).
 // B_COPIES: inside the loop group B issues every copy of a stage (the
 // dispatched kernel); otherwise each group copies its own share (the
 // persistent kernel, whose scalar registers are all in use: the extra LDS
 // addresses of the first scheme would spill).
-template <bool CAUSAL, int MAPPING, int ORDER, bool B_COPIES>
-__device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char *smem) {
+template <bool CAUSAL, bool B_COPIES>
+__device__ __forceinline__ void pp_tile(const KernelArgs &p, const Tile t, char *smem) {
     constexpr int D = 128;
     constexpr int BM = kBlockM128;
     constexpr int BN = kBlockN;
@@ -153,16 +152,6 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
     const int c = lane & 31;
     const int h = lane >> 5;
 
-    const Tile t = map_wid(MAPPING, ORDER, wid, p.B, p.Hq, p.NB, p.NX);
-    if (p.probe != nullptr && tid == 0) {
-        unsigned xcc;
-        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
-        int32_t *rec = p.probe + 4 * (int64_t)wid;
-        rec[0] = t.b;
-        rec[1] = t.hq;
-        rec[2] = t.m;
-        rec[3] = (int)(xcc & 0xf);
-    }
     const int g = t.hq / (p.Hq / p.Hkv);
     const int64_t q_head = ((int64_t)t.b * p.Hq + t.hq) * p.Sq * D;
     const int64_t kv_head = ((int64_t)t.b * p.Hkv + g) * p.Skv * D;
@@ -515,10 +504,43 @@ __device__ __forceinline__ void pp_tile(const KernelArgs &p, const int wid, char
     }
 }
 
+// With a probe buffer, thread 0 records (b, hq, m, XCC_ID) of workgroup `wid`
+// (for a paired slot, its first tile).
+__device__ __forceinline__ void record_probe(const KernelArgs &p, const int wid, const Tile t) {
+    if (p.probe != nullptr && threadIdx.x == 0) {
+        unsigned xcc;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+        int32_t *rec = p.probe + 4 * (int64_t)wid;
+        rec[0] = t.b;
+        rec[1] = t.hq;
+        rec[2] = t.m;
+        rec[3] = (int)(xcc & 0xf);
+    }
+}
+
+// One workgroup per tile or, with kOrderPaired in ORDER, per pair slot: the
+// slot's later (under a causal mask heavier) row block first, then its mirror.
 template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const KernelArgs p) {
     __shared__ __attribute__((aligned(1024))) char smem[kPPLdsBytes];
-    pp_tile<CAUSAL, MAPPING, ORDER, true>(p, blockIdx.x, smem);
+    const int wid = blockIdx.x;
+    if constexpr ((ORDER & kOrderPaired) != 0) {
+        Tile t = map_wid(MAPPING, ORDER, wid, p.B, p.Hq, pair_slots(p.NB), p.NX);
+        const int slot = t.m;
+        t.m = p.NB - 1 - slot;
+        record_probe(p, wid, t);
+        pp_tile<CAUSAL, true>(p, t, smem);
+        if (slot != t.m) {
+            // every wave is done with the first tile's LDS before the next copies land
+            __syncthreads();
+            t.m = slot;
+            pp_tile<CAUSAL, true>(p, t, smem);
+        }
+    } else {
+        const Tile t = map_wid(MAPPING, ORDER, wid, p.B, p.Hq, p.NB, p.NX);
+        record_probe(p, wid, t);
+        pp_tile<CAUSAL, true>(p, t, smem);
+    }
 }
 
 // Persistent form: one workgroup per CU takes tiles from per-XCD queues
@@ -530,7 +552,8 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_kernel(const Kernel
 // what is left in the others (so every tile is computed even if some XCD got
 // no workgroup).  The ticket for the next tile is requested when a tile
 // starts, so its latency hides behind the tile; the launch gap between
-// workgroups (about 5 us on MI355X) disappears.
+// workgroups (about 5 us on MI355X) disappears.  (The paired order is for
+// the dispatched grid only: the queues balance the work by themselves.)
 //
 // p.queue: kQueueInts int32, zero before the launch; the last workgroup to
 // finish sets it back to zero, so launches ordered on one stream can share it.
@@ -564,7 +587,9 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_persistent_kernel(c
     while (cur >= 0) {
         int pending = 0;
         if (threadIdx.x == 0) pending = atomicAdd(&queue[x], 1);   // result needed at the end
-        pp_tile<CAUSAL, MAPPING, ORDER, false>(p, cur, smem);
+        const Tile t = map_wid(MAPPING, ORDER, cur, p.B, p.Hq, p.NB, p.NX);
+        record_probe(p, cur, t);
+        pp_tile<CAUSAL, false>(p, t, smem);
         if (threadIdx.x == 0) next_wid = take(pending);
         __syncthreads();
         cur = next_wid;
@@ -584,9 +609,13 @@ __global__ __launch_bounds__(kPPThreads, 1) void attn_fwd_pp_persistent_kernel(c
 template <bool CAUSAL, int MAPPING, int ORDER>
 hipError_t launch_pp(const KernelArgs &a, int grid, hipStream_t stream) {
     if (a.queue != nullptr) {
-        hipLaunchKernelGGL((attn_fwd_pp_persistent_kernel<CAUSAL, MAPPING, ORDER>), dim3(grid),
-                           dim3(kPPThreads), 0, stream, a);
-        return hipGetLastError();
+        if constexpr ((ORDER & kOrderPaired) != 0) {
+            return hipErrorInvalidValue;   // no paired persistent form
+        } else {
+            hipLaunchKernelGGL((attn_fwd_pp_persistent_kernel<CAUSAL, MAPPING, ORDER>),
+                               dim3(grid), dim3(kPPThreads), 0, stream, a);
+            return hipGetLastError();
+        }
     }
     hipLaunchKernelGGL((attn_fwd_pp_kernel<CAUSAL, MAPPING, ORDER>), dim3(grid), dim3(kPPThreads),
                        0, stream, a);
@@ -594,23 +623,32 @@ hipError_t launch_pp(const KernelArgs &a, int grid, hipStream_t stream) {
 }
 
 // The block-major order inside an XCD's piece exists for mapping 2 only.
-template <bool CAUSAL, int MAPPING>
+template <bool CAUSAL, int MAPPING, int PAIRED>
 hipError_t launch_pp_order(const KernelArgs &a, int grid, hipStream_t stream) {
-    switch (MAPPING == ATTN_MAP_SWIZZLED_HEAD_FIRST ? a.order : (a.order & kOrderHeavyFirst)) {
-        case 0: return launch_pp<CAUSAL, MAPPING, 0>(a, grid, stream);
-        case 1: return launch_pp<CAUSAL, MAPPING, 1>(a, grid, stream);
-        case 2: return launch_pp<CAUSAL, MAPPING, (MAPPING == 2 ? 2 : 0)>(a, grid, stream);
-        default: return launch_pp<CAUSAL, MAPPING, (MAPPING == 2 ? 3 : 1)>(a, grid, stream);
-    }
+    constexpr int HF = kOrderHeavyFirst;
+    constexpr int BM = MAPPING == ATTN_MAP_SWIZZLED_HEAD_FIRST ? kOrderXcdBlockMajor : 0;
+    const bool hf = (a.order & HF) != 0;
+    if ((a.order & BM) != 0)
+        return hf ? launch_pp<CAUSAL, MAPPING, PAIRED | BM | HF>(a, grid, stream)
+                  : launch_pp<CAUSAL, MAPPING, PAIRED | BM>(a, grid, stream);
+    return hf ? launch_pp<CAUSAL, MAPPING, PAIRED | HF>(a, grid, stream)
+              : launch_pp<CAUSAL, MAPPING, PAIRED>(a, grid, stream);
+}
+
+template <bool CAUSAL, int MAPPING>
+hipError_t launch_pp_paired(const KernelArgs &a, int grid, hipStream_t stream) {
+    if ((a.order & kOrderPaired) != 0)
+        return launch_pp_order<CAUSAL, MAPPING, kOrderPaired>(a, grid, stream);
+    return launch_pp_order<CAUSAL, MAPPING, 0>(a, grid, stream);
 }
 
 template <bool CAUSAL>
 hipError_t launch_pp_mapping(const KernelArgs &a, int mapping, int grid, hipStream_t stream) {
     switch (mapping) {
-        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_pp_order<CAUSAL, 0>(a, grid, stream);
-        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_pp_order<CAUSAL, 1>(a, grid, stream);
-        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_pp_order<CAUSAL, 2>(a, grid, stream);
-        default: return launch_pp_order<CAUSAL, 3>(a, grid, stream);
+        case ATTN_MAP_NAIVE_BLOCK_FIRST: return launch_pp_paired<CAUSAL, 0>(a, grid, stream);
+        case ATTN_MAP_NAIVE_HEAD_FIRST: return launch_pp_paired<CAUSAL, 1>(a, grid, stream);
+        case ATTN_MAP_SWIZZLED_HEAD_FIRST: return launch_pp_paired<CAUSAL, 2>(a, grid, stream);
+        default: return launch_pp_paired<CAUSAL, 3>(a, grid, stream);
     }
 }
 

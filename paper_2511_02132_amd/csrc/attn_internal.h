@@ -43,9 +43,19 @@ constexpr int kQueueMaxXcd = 32;
 constexpr int kQueueDone = kQueueMaxXcd;
 constexpr int kQueueInts = 64;
 
-// Order bits (from ATTN_ORDER_HEAVY_FIRST and ATTN_ORDER_XCD_BLOCK_MAJOR).
+// Order bits (from ATTN_ORDER_HEAVY_FIRST, ATTN_ORDER_XCD_BLOCK_MAJOR and
+// ATTN_ORDER_PAIRED).
 constexpr int kOrderHeavyFirst = 1;
 constexpr int kOrderXcdBlockMajor = 2;
+// Paired row blocks (head dimension 128, forward): the grid has
+// pair_slots(NB) slots per head instead of NB row blocks; map_wid decodes a
+// workgroup id over (B, Hq, pair_slots(NB)) with the other order bits, and
+// slot p computes row block NB-1-p and then row block p (once, when the two
+// coincide).  Under a causal mask with Sq == Skv every pair costs the same
+// NB+1 block-widths of K/V (the middle block of an odd NB costs about half).
+constexpr int kOrderPaired = 4;
+
+__host__ __device__ constexpr int pair_slots(int NB) { return (NB + 1) / 2; }
 // Heads per block-major group: one per shader engine of an XCD; for heads of
 // at most kShortHeadBlocks row blocks, kBlockMajorHeadsShort.
 constexpr int kBlockMajorHeads = 4;

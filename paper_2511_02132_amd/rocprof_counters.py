@@ -32,12 +32,14 @@ MAPPING_NAMES = ["naive_block_first", "naive_head_first", "swizzled_head_first",
                  "swizzled_block_first"]
 # attn_fwd_kernel<d, stored d, causal, mapping, order> (4-wave kernel) and
 # attn_fwd_pp_kernel<causal, mapping, order> (d = 128 two-group kernel); order
-# bit 0 = heavy-first, bit 1 = block-major inside each XCD's piece
+# bit 0 = heavy-first, bit 1 = block-major inside each XCD's piece, bit 2 =
+# paired row blocks
 KERNEL_RE = re.compile(r"attn_fwd_(?:kernel<\d+, \d+, |pp_kernel<)(true|false), (\d), (\d)>")
 
 
 def order_suffix(order: int) -> str:
-    return ("+heavy_first" if order & 1 else "") + ("+xcd_block_major" if order & 2 else "")
+    return ("+heavy_first" if order & 1 else "") + ("+xcd_block_major" if order & 2 else "") + \
+        ("+paired" if order & 4 else "")
 
 
 def variant_of(kernel_name: str):

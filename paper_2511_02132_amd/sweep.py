@@ -50,9 +50,9 @@ GQA_KV_HEADS = 8
 D = 128
 
 
-def variants(causal: bool):
+def variants(causal: bool, d: int = D, backward: bool = False):
     import paper_2511_02132_amd as pa
-    return pa.variants(causal)
+    return pa.variants(causal, d, backward)
 
 
 def configs(family: str, contexts, batches, heads, kv_heads=GQA_KV_HEADS):
@@ -143,7 +143,7 @@ def run(a):
     stream = torch.cuda.current_stream(dev)
     flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device=dev)
     gen = torch.Generator(device=dev)
-    vs = variants(causal)
+    vs = variants(causal, a.d, a.which == "bwd")
     manifest = []
     out = open(a.json, "a") if a.json else None
     for ci, c in enumerate(configs(a.family, a.contexts, a.batches, a.heads, a.kv_heads)):
@@ -332,12 +332,16 @@ def comparisons(recs, names, sh, causal):
     if causal:
         pairs.append(("swizzled_head_first+heavy_first", "naive_block_first+heavy_first",
                       "same (heavy-first) block order"))
+        pairs.append(("swizzled_head_first+heavy_first+paired",
+                      "naive_block_first+heavy_first+paired", "same (paired) block order"))
     best_bf = [n for n in ("naive_block_first", "swizzled_block_first") + (
-        ("naive_block_first+heavy_first", "swizzled_block_first+heavy_first") if causal else ())
-        if n in names]
+        ("naive_block_first+heavy_first", "swizzled_block_first+heavy_first",
+         "naive_block_first+heavy_first+paired", "swizzled_block_first+heavy_first+paired")
+        if causal else ()) if n in names]
     heads = [n for n in ("swizzled_head_first+heavy_first" if causal else "swizzled_head_first",
                          "swizzled_head_first+heavy_first+xcd_block_major" if causal else
-                         "swizzled_head_first+xcd_block_major") if n in names]
+                         "swizzled_head_first+xcd_block_major",
+                         "swizzled_head_first+heavy_first+paired") if n in names]
     out += ["| comparison | wins | ties | losses | losses (ratio of medians) |", "|---|---|---|---|---|"]
 
     def row(label, res):
@@ -378,21 +382,21 @@ def summarise(a):
     l2 = l2_by_launch(a.counters, a.manifest) if a.counters else {}
     l2r = l2_read_bounds_by_launch(a.counters, a.manifest) if a.counters else {}
     causal = recs[0]["causal"] if recs else True
-    names = [n for n, _ in variants(causal)]
+    which = recs[0].get("pass", "fwd") if recs else "fwd"
+    names = [n for n, _ in variants(causal, recs[0].get("d", D) if recs else D, which == "bwd")]
     short = {"naive_block_first": "NBF", "naive_head_first": "NHF", "swizzled_head_first": "SHF",
              "swizzled_block_first": "SBF"}
 
     def sh(n):
         parts = n.split("+")
         return short[parts[0]] + ("+hf" if "heavy_first" in parts else "") + \
-            ("+bm" if "xcd_block_major" in parts else "")
+            ("+bm" if "xcd_block_major" in parts else "") + ("+p" if "paired" in parts else "")
 
     import paper_2511_02132_amd as pa
     base = pa.variant_name(pa.method_variant(causal))
     if recs and base not in recs[0]["tflops"]:   # records taken before the block-major order
         base = "swizzled_head_first" + ("+heavy_first" if causal else "")
     names = [n for n in names if not recs or n in recs[0]["tflops"]]
-    which = recs[0].get("pass", "fwd") if recs else "fwd"
     lines = ["# Mapping sweep: %s %s, d=%d, %s" % (
         recs[0]["family"].upper() if recs else "?", "backward" if which == "bwd" else "forward",
         recs[0].get("d", D) if recs else D, "causal" if causal else "non-causal"), ""]
@@ -410,7 +414,8 @@ def summarise(a):
                   "TCC_READ, TCC_WRITE: between no write hitting and every write hitting)."]
     lines += ["", "Variants: NBF naive block-first, NHF naive head-first, SHF swizzled head-first "
               "(the method), SBF swizzled block-first; +hf = heavy-first block order, +bm = "
-              "block-major order in groups of four heads inside each XCD's piece.", ""]
+              "block-major order in groups of four heads inside each XCD's piece, +p = paired "
+              "row blocks (one workgroup per pair NB-1-p, p of a head).", ""]
     if a.note:
         lines += [a.note, ""]
     if a.cmd:

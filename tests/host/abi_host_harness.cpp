@@ -149,7 +149,12 @@ void check_validation() {
         {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 0, 2, ATTN_ERR_SHAPE},
         {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 4, ATTN_ERR_MAPPING},
         {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, -1, ATTN_ERR_MAPPING},
-        {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 0x42, ATTN_ERR_MAPPING},
+        {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 0x82, ATTN_ERR_MAPPING},
+        {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 0x100, ATTN_ERR_MAPPING},
+        {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 0x61, ATTN_ERR_MAPPING},
+        // paired row blocks: head dimension 128 only
+        {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 64, 0x42, ATTN_ERR_UNSUPPORTED},
+        {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 56, 0x52, ATTN_ERR_UNSUPPORTED},
         {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 0x20, ATTN_ERR_MAPPING},
         {kQ, kK, kV, kO, 1, 4, 2, 256, 256, 128, 0x33, ATTN_ERR_MAPPING},
         {kQ + 8, kK, kV, kO, 1, 4, 2, 256, 256, 128, 2, ATTN_ERR_ALIGN},
@@ -188,6 +193,10 @@ void check_forward_launch() {
         {1, 2, 2, 517, 333, 56, 1, 0x32},  {2, 6, 3, 129, 65, 64, 0, 0x13},
         {1, 1, 1, 1, 1, 128, 0, 1},        {3, 5, 5, 1000, 64, 56, 1, 0x22},
         {1, 16, 16, 131072, 131072, 128, 1, 0x12},
+        // paired row blocks: ceil(NB/2) slots per head
+        {1, 16, 16, 131072, 131072, 128, 1, 0x52}, {2, 8, 2, 384, 384, 128, 1, 0x40},
+        {1, 3, 1, 1300, 1300, 128, 1, 0x53},       {1, 2, 2, 1, 1, 128, 0, 0x41},
+        {2, 4, 4, 700, 900, 128, 0, 0x62},
     };
     for (const Shape &s : shapes) {
         const int before = g_fwd_launches;
@@ -199,14 +208,16 @@ void check_forward_launch() {
         const int nb = (s.Sq + bm - 1) / bm;
         CHECK(attn_block_m(s.d) == bm);
         CHECK(g_fwd.NB == nb);
-        CHECK(g_fwd_grid == s.B * s.Hq * nb);
-        CHECK(attn_grid_size(s.B, s.Hq, s.Sq, s.d) == (int64_t)g_fwd_grid);
+        const bool paired = (s.mapping & 0x40) != 0;
+        CHECK(g_fwd_grid == s.B * s.Hq * (paired ? (nb + 1) / 2 : nb));
+        CHECK(attn_grid_size(s.B, s.Hq, s.Sq, s.d) == (int64_t)s.B * s.Hq * nb);
         CHECK(g_fwd.B == s.B && g_fwd.Hq == s.Hq && g_fwd.Hkv == s.Hkv);
         CHECK(g_fwd.Sq == s.Sq && g_fwd.Skv == s.Skv);
         CHECK(g_fwd_d == s.d && g_fwd_causal == (s.causal != 0));
         CHECK(g_fwd_mapping == (s.mapping & 0xf));
         CHECK(g_fwd.order == (((s.mapping & 0x10) ? attn::kOrderHeavyFirst : 0) |
-                              ((s.mapping & 0x20) ? attn::kOrderXcdBlockMajor : 0)));
+                              ((s.mapping & 0x20) ? attn::kOrderXcdBlockMajor : 0) |
+                              (paired ? attn::kOrderPaired : 0)));
         CHECK(g_fwd.NX == 8);
         CHECK(std::fabs(g_fwd.scale_log2 - scale * 1.44269504f) <= 1e-6f * scale);
         CHECK(g_fwd.q == P(kQ) && g_fwd.k == P(kK) && g_fwd.v == P(kV) && g_fwd.o == P(kO));
@@ -237,6 +248,12 @@ void check_lse_probe() {
     CHECK(attn_fwd_probe(P(kQ), P(kK), P(kV), P(kO), 1, 4, 2, 300, 300, 64, 0, 0.1f, 3, probe) ==
           ATTN_OK);
     CHECK(g_fwd.probe == probe && g_fwd.lse == nullptr && g_fwd_grid == 4 * 3);
+    // paired: the probe covers the ceil(NB/2) slots of each head
+    CHECK(attn_fwd_probe(P(kQ), P(kK), P(kV), P(kO), 1, 4, 2, 1300, 1300, 128, 1, 0.1f, 0x52,
+                         probe) == ATTN_OK);
+    CHECK(g_fwd.probe == probe && g_fwd_grid == 4 * 3 && g_fwd.NB == 6);
+    CHECK(attn_fwd_lse(P(kQ), P(kK), P(kV), P(kO), lse, 1, 4, 2, 300, 300, 64, 1, 0.1f, 0x42) ==
+          ATTN_ERR_UNSUPPORTED);
 }
 
 void check_persistent() {
@@ -250,6 +267,9 @@ void check_persistent() {
     CHECK(pers((int32_t *)P(kW + 2), nullptr, 1, 4, 4, 512, 128) == ATTN_ERR_ALIGN);
     CHECK(pers(queue, (int32_t *)P(kP + 2), 1, 4, 4, 512, 128) == ATTN_ERR_ALIGN);
     CHECK(pers(queue, nullptr, 1, 4, 4, 512, 64) == ATTN_ERR_UNSUPPORTED);
+    // paired row blocks are for the dispatched grid only
+    CHECK(attn_fwd_persistent(P(kQ), P(kK), P(kV), P(kO), lse, queue, nullptr, 1, 4, 4, 512, 512,
+                              128, 1, 0.088f, 0x52) == ATTN_ERR_UNSUPPORTED);
     CHECK(pers((int32_t *)P(kO + 1024), nullptr, 1, 4, 4, 512, 128) == ATTN_ERR_ALIAS);
     CHECK(pers((int32_t *)P(kL), nullptr, 1, 4, 4, 512, 128) == ATTN_ERR_ALIAS);
     // the queue ends exactly where q starts: no overlap
@@ -275,6 +295,8 @@ void check_persistent() {
     CHECK(noalloc((int32_t *)P(kP + 2), 1, 4, 4, 512, 128, kO) == ATTN_ERR_ALIGN);
     CHECK(noalloc(nullptr, 1, 4, 4, 512, 128, kQ) == ATTN_ERR_ALIAS);
     CHECK(noalloc(nullptr, 1, 4, 3, 512, 128, kO) == ATTN_ERR_SHAPE);
+    CHECK(attn_fwd_persistent_noalloc(P(kQ), P(kK), P(kV), P(kO), lse, nullptr, 1, 4, 4, 512, 512,
+                                      128, 1, 0.088f, 0x42) == ATTN_ERR_UNSUPPORTED);
     setenv("ATTN_NUM_XCD", "33", 1);
     CHECK(noalloc(nullptr, 1, 4, 4, 512, 128, kO) == ATTN_ERR_UNSUPPORTED);
     unsetenv("ATTN_NUM_XCD");
@@ -298,6 +320,9 @@ void check_backward() {
     CHECK(g_bwd.NBQ == 3 && g_bwd.NKV == 4 && g_bwd.NX == 8 && g_bwd_mapping == 2 && g_bwd_causal);
     CHECK(g_bwd.order == attn::kOrderHeavyFirst && g_bwd.delta == (float *)P(kG));
     CHECK(bwd(ins, outs, 64, 2, 8, 2, 300, 500) == ATTN_ERR_UNSUPPORTED);
+    // paired row blocks: a forward-only order
+    CHECK(attn_bwd(P(kQ), P(kK), P(kV), P(kO), P(kD), (const float *)P(kL), (float *)P(kG), P(kX),
+                   P(kY), P(kZ), 2, 8, 2, 300, 500, 128, 1, 0.088f, 0x52) == ATTN_ERR_MAPPING);
     for (int i = 0; i < 6; ++i) {   // a null input
         uintptr_t in[6];
         std::memcpy(in, ins, sizeof in);
@@ -385,14 +410,22 @@ void write_map_tables(const char *path) {
         {1, 1, 1, 128, 8},    {2, 3, 129, 64, 1},    {1, 7, 1700, 128, 3}, {2, 128, 2048, 56, 8},
         {4, 6, 513, 128, 8},  {1, 64, 2176, 64, 8},  {3, 9, 4000, 128, 5},
     };
-    const int values[] = {0, 1, 2, 3, 0x10, 0x11, 0x12, 0x13, 0x22, 0x32};
+    // each value also with paired row blocks (head dimension 128 only)
+    const int values[] = {0,    1,    2,    3,    0x10, 0x11, 0x12, 0x13, 0x22, 0x32,
+                          0x40, 0x41, 0x42, 0x43, 0x50, 0x51, 0x52, 0x53, 0x62, 0x72};
     FILE *f = std::fopen(path, "wb");
     CHECK(f != nullptr);
     for (const auto &s : shapes) {
         for (int value : values) {
             const int64_t n = attn_grid_size(s[0], s[1], s[2], s[3]);
             CHECK(n > 0);
-            std::vector<int32_t> out((size_t)n * 3, -1);
+            // a sentinel no entry can hold: every row must be written
+            std::vector<int32_t> out((size_t)n * 3, 0x7eadbeef);
+            if ((value & 0x40) && s[3] != 128) {
+                CHECK(attn_map_tiles(value, s[0], s[1], s[2], s[3], s[4], out.data()) ==
+                      ATTN_ERR_UNSUPPORTED);
+                continue;
+            }
             CHECK(attn_map_tiles(value, s[0], s[1], s[2], s[3], s[4], out.data()) == ATTN_OK);
             const int32_t hdr[6] = {value, s[0], s[1], s[2], s[3], s[4]};
             CHECK(std::fwrite(hdr, sizeof hdr, 1, f) == 1);

@@ -51,7 +51,9 @@ def call(q=Q, k=K, v=V, o=O, B=1, Hq=4, Hkv=2, Sq=256, Skv=256, d=128, causal=0,
     (dict(B=0), -2), (dict(Hq=0), -2), (dict(Hkv=0), -2), (dict(Sq=0), -2), (dict(Skv=-1), -2),
     (dict(Hq=6, Hkv=4), -2), (dict(Sq=2 ** 23), -2), (dict(Skv=2 ** 23), -2),
     (dict(d=96), -3), (dict(d=256), -3), (dict(d=0), -2),
-    (dict(mapping=4), -4), (dict(mapping=-1), -4), (dict(mapping=0x40 | 2), -4),
+    (dict(mapping=4), -4), (dict(mapping=-1), -4), (dict(mapping=0x80 | 2), -4),
+    # paired row blocks exist for d = 128 only
+    (dict(mapping=0x40 | 2, d=64), -3), (dict(mapping=0x50 | 0, d=56), -3),
     (dict(mapping=0x14), -4), (dict(mapping=0xf), -4),
     # the block-major order inside an XCD's piece exists for swizzled head-first only
     (dict(mapping=0x20 | 0), -4), (dict(mapping=0x20 | 1), -4), (dict(mapping=0x30 | 3), -4),
@@ -109,13 +111,20 @@ MAP_SHAPES = [(1, 4, 256, 64, 8), (1, 32, 8192, 128, 8), (1, 64, 8192, 128, 8),
 @pytest.mark.parametrize("B,Hq,Sq,d,NX", MAP_SHAPES)
 def test_library_mapping_equals_oracle(B, Hq, Sq, d, NX):
     BM = pa.block_m(d)
-    for value in [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]:
-        mapping, heavy, xbm = mp.split_flags(value)
+    values = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]
+    for value in values + [v | pa.PAIRED for v in values]:
+        mapping, heavy, xbm, paired = mp.split_flags(value)
+        if paired and d != 128:
+            with pytest.raises(pa.AttnError) as e:
+                pa.map_tiles(value, B, Hq, Sq, d, NX)
+            assert e.value.code == -3
+            continue
         got = pa.map_tiles(value, B, Hq, Sq, d, NX)
         want = mp.enumerate_mapping(mapping, B, Hq, Sq, BM, NX, heavy_first=heavy,
                                     short_head_groups=(BM == 128),
-                                    xcd_block_major=xbm)
-        assert np.array_equal(got, want), hex(value)
+                                    xcd_block_major=xbm, paired=paired)
+        assert np.array_equal(got[:want.shape[0]], want), hex(value)
+        assert (got[want.shape[0]:] == -1).all(), hex(value)
 
 
 def test_map_tiles_errors():
@@ -124,6 +133,8 @@ def test_map_tiles_errors():
     ptr = out.ctypes.data_as(pa._i32p)
     assert pa.lib().attn_map_tiles(5, 1, 4, 256, 64, 8, ptr) == -4
     assert pa.lib().attn_map_tiles(2, 1, 4, 256, 64, 0, ptr) == -2
+    assert pa.lib().attn_map_tiles(2 | pa.PAIRED, 1, 4, 256, 64, 8, ptr) == -3   # d = 128 only
+    assert pa.lib().attn_map_tiles(2 | 0x80, 1, 4, 256, 128, 8, ptr) == -4
 
 
 def test_calib_validation():

@@ -56,9 +56,12 @@ def test_abi_host_code_under_sanitizers(tmp_path):
         n = B * Hq * ((Sq + BM - 1) // BM)
         got = data[pos:pos + 3 * n].reshape(n, 3)
         pos += 3 * n
-        mapping, heavy, xbm = mp.split_flags(value)
+        mapping, heavy, xbm, paired = mp.split_flags(value)
         want = mp.enumerate_mapping(mapping, B, Hq, Sq, BM, NX, heavy_first=heavy,
-                                    short_head_groups=(BM == 128), xcd_block_major=xbm)
+                                    short_head_groups=(BM == 128), xcd_block_major=xbm,
+                                    paired=paired)
+        # the rows past the paired grid hold -1
+        want = np.concatenate([want, np.full((n - want.shape[0], 3), -1)])
         assert np.array_equal(got, want), (hex(value), B, Hq, Sq, d, NX)
         cases += 1
-    assert cases == 11 * 10
+    assert cases == 11 * 10 + 6 * 10   # six shapes have d = 128 and also take the paired order

@@ -24,6 +24,11 @@ pytestmark = pytest.mark.gpu
 # and swizzled head-first with block-major order inside each XCD's piece
 ALL_MAPPINGS = [m | f for m in (0, 1, 2, 3) for f in (0, 0x10)] + [0x22, 0x32]
 
+
+def mappings_for(d):
+    """ALL_MAPPINGS and, for d = 128, each of them also with paired row blocks."""
+    return ALL_MAPPINGS + ([m | pa.PAIRED for m in ALL_MAPPINGS] if d == 128 else [])
+
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
 DEV = "cuda:0"
@@ -70,17 +75,19 @@ def test_probe_matches_enumeration_and_dispatch(B, Hq, Hkv, S, d):
     nx = pa.num_xcd()
     BM = pa.block_m(d)
     outs = []
-    for value in ALL_MAPPINGS:
-        mapping, heavy, xbm = mp.split_flags(value)
+    for value in mappings_for(d):
+        mapping, heavy, xbm, paired = mp.split_flags(value)
         o, probe = pa.attn_fwd_probe(q, k, v, causal=True, mapping=value)
         torch.cuda.synchronize()
         rec = probe.cpu().numpy()
         want = mp.enumerate_mapping(mapping, B, Hq, S, BM, nx, heavy_first=heavy,
                                     short_head_groups=(BM == 128),
-                                    xcd_block_major=xbm)
-        assert np.array_equal(rec[:, :3], want), "placement differs from the enumeration"
-        wid = np.arange(rec.shape[0])
-        assert np.array_equal(rec[:, 3], wid % nx), "XCC_ID != wid mod NX"
+                                    xcd_block_major=xbm, paired=paired)
+        n = want.shape[0]   # workgroups launched (pair slots when paired)
+        assert np.array_equal(rec[:n, :3], want), "placement differs from the enumeration"
+        assert (rec[n:] == -1).all(), "a record past the paired grid was written"
+        wid = np.arange(n)
+        assert np.array_equal(rec[:n, 3], wid % nx), "XCC_ID != wid mod NX"
         outs.append(o)
     for o in outs[1:]:
         assert torch.equal(o, outs[0]), "output depends on the mapping"
@@ -119,7 +126,7 @@ def test_parity_small(B, Hq, Hkv, Sq, Skv, d, causal):
     scale = ai.default_scale(d)
     ref = oracle.attn_fwd_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), causal, scale)
     qd, kd, vd = _to_dev(q, k, v)
-    outs = [_run(qd, kd, vd, causal, scale, m) for m in ALL_MAPPINGS]
+    outs = [_run(qd, kd, vd, causal, scale, m) for m in mappings_for(d)]
     for o in outs:
         assert not torch.isnan(o).any(), "unwritten output elements"
         mx, mean = _err(o, ref)
@@ -183,6 +190,11 @@ def test_errors_surface_as_exceptions():
     with pytest.raises(pa.AttnError) as e:
         pa.attn_fwd(q, q, q, q)
     assert e.value.code == -8
+    # paired row blocks: the d = 128 dispatched forward only
+    q64 = torch.zeros(1, 2, 128, 64, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(pa.AttnError) as e:
+        pa.attn_fwd(q64, q64, q64, mapping=pa.SWIZZLED_HEAD_FIRST | pa.PAIRED)
+    assert e.value.code == -3
 
 
 # ------------------------------------------------------------------ full sizes, sampled rows
@@ -199,7 +211,7 @@ def test_parity_full_size_sampled_rows(name):
     scale = ai.default_scale(w["d"])
     causal = w["causal"]
     qd, kd, vd = _to_dev(q, k, v)
-    outs = [_run(qd, kd, vd, causal, scale, m) for m in ALL_MAPPINGS]
+    outs = [_run(qd, kd, vd, causal, scale, m) for m in mappings_for(w["d"])]
     for o in outs:
         assert not torch.isnan(o).any(), "unwritten output elements"
     for o in outs[1:]:
@@ -315,7 +327,8 @@ def test_forward_lse_all_head_dims(B, Hq, Hkv, Sq, Skv, d, causal):
     scale = ai.default_scale(d)
     qd, kd, vd = _to_dev(q, k, v)
     lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float32, device=DEV)
-    for m in (pa.SWIZZLED_HEAD_FIRST, pa.method_variant(causal), pa.NAIVE_BLOCK_FIRST):
+    paired = (pa.method_variant(causal) | pa.PAIRED,) if d == 128 else ()
+    for m in (pa.SWIZZLED_HEAD_FIRST, pa.method_variant(causal), pa.NAIVE_BLOCK_FIRST) + paired:
         o, lse = pa.attn_fwd_lse(qd, kd, vd, lse=lse, causal=causal, scale=scale, mapping=m)
         torch.cuda.synchronize()
         ref, _ = oracle.attn_row_stats_f64(ai.bf16_bits(q), ai.bf16_bits(k), ai.bf16_bits(v), None,

@@ -172,4 +172,7 @@ def test_backward_errors():
     with pytest.raises(pa.AttnError) as e:
         pa.attn_bwd(q, k, v, o, do, lse, mapping=7)
     assert e.value.code == -4
+    with pytest.raises(pa.AttnError) as e:   # paired row blocks: a forward-only order
+        pa.attn_bwd(q, k, v, o, do, lse, mapping=pa.SWIZZLED_HEAD_FIRST | pa.PAIRED)
+    assert e.value.code == -4
     torch.cuda.synchronize()

@@ -133,7 +133,7 @@ def test_persistent_equals_dispatched(B, Hq, Hkv, Sq, Skv, causal):
     ref_o, ref_lse = pa.attn_fwd_lse(q, k, v, causal=causal, scale=scale)
     torch.cuda.synchronize()
     for value in VARIANTS:
-        mapping, heavy, xbm = mp.split_flags(value)
+        mapping, heavy, xbm, _ = mp.split_flags(value)
         o = torch.full_like(q, float("nan"))
         lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float32, device=DEV)
         probe = torch.full((n, 4), -1, dtype=torch.int32, device=DEV)
@@ -178,4 +178,7 @@ def test_persistent_errors():
         o = torch.empty_like(q)
         pa.attn_fwd_persistent(q, k, v, o, queue=o.view(torch.int32).view(-1)[:64])
     assert e.value.code == -8
+    with pytest.raises(pa.AttnError) as e:   # paired row blocks: dispatched grid only
+        pa.attn_fwd_persistent(q, k, v, mapping=pa.SWIZZLED_HEAD_FIRST | pa.PAIRED)
+    assert e.value.code == -3
     torch.cuda.synchronize()

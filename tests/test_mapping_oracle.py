@@ -19,7 +19,11 @@ What ties the enumeration (oracle/mapping.py) to the paper:
     pieces in head-major order;
   * swizzled block-first (Section 3.2) keeps the block-major order, puts each
     GQA group on one XCD when the group count equals NX, serves Hq/NX heads
-    per row block on each XCD for MHA, and is naive block-first when NX = 1.
+    per row block on each XCD for MHA, and is naive block-first when NX = 1;
+  * paired row blocks (an order option): hand-worked tables, every tile
+    computed once, every slot of equal causal cost but one middle block per
+    head, one ACC at a time, and equal work per shader engine where
+    heavy-first order alone leaves it unequal.
 Planted mistakes in the enumeration (monkeypatched) must fail a pin.
 """
 
@@ -238,9 +242,70 @@ def pin_heavy_first_order(m):
     assert all(v == sorted(v, reverse=True) and len(v) == NB for v in seen.values())
 
 
+def pin_paired(m):
+    """Order option: one WG per slot p of a head computes row blocks NB-1-p, then p."""
+    # worked by hand: B=1, Hq=2, NB=5 (three slots per head), NX=2, swizzled
+    # head-first.  XCD 0 takes head 0's slots, XCD 1 head 1's; slot p first
+    # computes block 4-p (blocks 4+0, 3+1, then the middle block 2 alone).
+    t = [m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, 1, 2, 5, 2, paired=True) for w in range(6)]
+    assert t == [(0, 0, 4), (0, 1, 4), (0, 0, 3), (0, 1, 3), (0, 0, 2), (0, 1, 2)]
+    # the same with heavy-first order: the slots of each head in reverse
+    t = [m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, 1, 2, 5, 2, True, paired=True) for w in range(6)]
+    assert t == [(0, 0, 2), (0, 1, 2), (0, 0, 3), (0, 1, 3), (0, 0, 4), (0, 1, 4)]
+    # naive block-first, B=1, Hq=3, NB=4: slot 0 of every head, then slot 1
+    t = [m.map_wid(mp.NAIVE_BLOCK_FIRST, w, 1, 3, 4, 8, paired=True) for w in range(6)]
+    assert t == [(0, 0, 3), (0, 1, 3), (0, 2, 3), (0, 0, 2), (0, 1, 2), (0, 2, 2)]
+    assert [m.slot_blocks(mm, 5) for mm in (4, 3, 2)] == [[4, 0], [3, 1], [2]]
+    for (B, Hq, NB, NX) in SHAPES[::5] + [(1, 32, 32, 8), (1, 16, 512, 8), (2, 12, 3, 8)]:
+        for mapping in mp.MAPPINGS:
+            for heavy, xbm in ((False, False), (True, False), (True, True)):
+                if xbm and mapping != mp.SWIZZLED_HEAD_FIRST:
+                    continue
+                n = B * Hq * ((NB + 1) // 2)   # ceil(NB / 2) slots per head
+                with pytest.raises(ValueError):
+                    m.map_wid(mapping, n, B, Hq, NB, NX, heavy, xbm, paired=True)
+                seen = []
+                costs = []
+                for w in range(n):
+                    b, hq, first = m.map_wid(mapping, w, B, Hq, NB, NX, heavy, xbm, paired=True)
+                    blocks = m.slot_blocks(first, NB)
+                    assert blocks[0] == max(blocks), "the later block first"
+                    seen += [(b, hq, blk) for blk in blocks]
+                    costs.append(sum(blk + 1 for blk in blocks))   # causal: block m costs m+1
+                # every tile of the grid exactly once
+                assert sorted(seen) == [(b, h, k) for b in range(B) for h in range(Hq)
+                                        for k in range(NB)], (mapping, B, Hq, NB, NX)
+                # every slot costs NB+1, except one middle block per head when NB is odd
+                odd = [c for c in costs if c != NB + 1]
+                assert len(odd) == (B * Hq if NB % 2 else 0)
+                assert all(c == (NB + 1) // 2 for c in odd)
+    # one ACC at a time (Section 3.3) still holds for swizzled head-first
+    for (B, Hq, Hkv, NB) in [(1, 32, 32, 32), (1, 64, 8, 32), (1, 16, 16, 512), (2, 16, 4, 9)]:
+        n = B * Hq * ((NB + 1) // 2)
+        t = np.array([m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, 8, True, paired=True)
+                      for w in range(n)])
+        owner = {}
+        for x, seq in enumerate(m.xcd_acc_sequences(t, Hq, Hkv, 8)):
+            assert all(a <= c for a, c in zip(seq, seq[1:]))
+            for a in seq:
+                assert owner.setdefault(a, x) == x, "ACC split across XCDs"
+    # shader-engine balance (the reason for the order): the k-th WG of an XCD
+    # goes to engine k mod 4; on MHA B1 H32 with 32 row blocks each engine of
+    # each XCD gets the same causal work, which heavy-first alone does not give
+    B, Hq, NB, NX = 1, 32, 32, 8
+    for paired, balanced in ((True, True), (False, False)):
+        n = B * Hq * (((NB + 1) // 2) if paired else NB)
+        work = np.zeros((NX, 4))
+        for w in range(n):
+            _, _, first = m.map_wid(mp.SWIZZLED_HEAD_FIRST, w, B, Hq, NB, NX, True, paired=paired)
+            blocks = m.slot_blocks(first, NB) if paired else [first]
+            work[w % NX, (w // NX) % 4] += sum(blk + 1 for blk in blocks)
+        assert (work.max(axis=1) == work.min(axis=1)).all() == balanced
+
+
 PINS = [pin_heavy_first_order, pin_permutation, pin_chiplet_swizzle, pin_head_first_listing, pin_caption_example,
         pin_one_acc_at_a_time, pin_gqa_groups_on_one_xcd, pin_swizzled_block_first,
-        pin_xcd_block_major, pin_ceil_blocks]
+        pin_xcd_block_major, pin_ceil_blocks, pin_paired]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -274,7 +339,11 @@ class _Mutant:
         me = self
 
         def map_wid(mapping, wid, B, Hq, NB, NX, heavy_first=False, xcd_block_major=False,
-                    short_head_groups=False):
+                    short_head_groups=False, paired=False):
+            if paired:
+                b, hq, p = me.paired_slot(mapping, wid, B, Hq, NB, NX, heavy_first,
+                                          xcd_block_major, short_head_groups)
+                return b, hq, me.pair_first(p, NB)
             N = B * Hq * NB
             if not 0 <= wid < N:
                 raise ValueError("wid out of range")
@@ -300,6 +369,10 @@ class _Mutant:
         self.__dict__.setdefault("reverse_block", lambda mm, NB: NB - 1 - mm)
         self.__dict__.setdefault("sbf_head", lambda j, Hq, NX: me.swizzled_rank(j, Hq, NX))
         self.__dict__.setdefault("bm_rank", _bm_rank)
+        self.__dict__.setdefault("pair_first", lambda p, NB: NB - 1 - p)
+        self.__dict__.setdefault(
+            "paired_slot", lambda mapping, wid, B, Hq, NB, NX, hf, xbm, sh: me.map_wid(
+                mapping, wid, B, Hq, me.pair_slots(NB), NX, hf, xbm, sh))
 
 
 def _bm_rank(L, x, N, NX, NB, short=False, G=4, max_blocks=64, G_short=16, short_blocks=16,
@@ -404,6 +477,15 @@ MAP_MUTANTS = {
         L, x, N, NX, NB, sh, short_blocks=15)),
     "block_major_short_groups_always": dict(bm_rank=lambda L, x, N, NX, NB, sh=False: _bm_rank(
         L, x, N, NX, NB, sh, ignore_flag=True)),
+    "paired_slots_floor": dict(pair_slots=lambda NB: NB // 2),
+    "paired_first_is_the_slot": dict(pair_first=lambda p, NB: p),
+    "paired_mirror_off_by_one": dict(
+        slot_blocks=lambda mm, NB: [mm] if NB - mm == mm else [mm, NB - mm]),
+    "paired_order_flags_dropped": dict(paired_slot=lambda mapping, wid, B, Hq, NB, NX, hf, xbm, sh:
+                                       mp.map_wid(mapping, wid, B, Hq, (NB + 1) // 2, NX)),
+    "paired_slots_decoded_over_all_blocks": dict(
+        paired_slot=lambda mapping, wid, B, Hq, NB, NX, hf, xbm, sh: mp.map_wid(
+            mapping, wid, B, Hq, NB, NX, hf, xbm, sh)),
     "block_first_swizzle_transposed": dict(
         sbf_head=lambda j, Hq, NX: (j % (Hq // NX if Hq >= NX else 1)) * NX + j // max(Hq // NX, 1)
         if Hq % NX == 0 else j),

@@ -21,7 +21,8 @@ from paper_2511_02132_amd import sweep  # noqa: E402
 
 
 def _order_bits(mapping):
-    return (1 if mapping & pa.HEAVY_FIRST else 0) | (2 if mapping & pa.XCD_BLOCK_MAJOR else 0)
+    return (1 if mapping & pa.HEAVY_FIRST else 0) | (2 if mapping & pa.XCD_BLOCK_MAJOR else 0) | \
+        (4 if mapping & pa.PAIRED else 0)
 
 
 def test_variant_of_kernel_names():
@@ -244,6 +245,8 @@ def test_sweep_spread_comparisons():
         ms = {n: 1.0 for n in names}
         ms["naive_block_first+heavy_first"] = slow          # vs the headline: win, tie, loss
         ms["swizzled_block_first+heavy_first"] = 1.2
+        ms["naive_block_first+heavy_first+paired"] = 1.2
+        ms["swizzled_block_first+heavy_first+paired"] = 1.2
         ms["naive_block_first"] = ms["swizzled_block_first"] = 1.3
         recs.append({"S": 8192 * (i + 1), "B": 1, "Hq": 32, "Hkv": 32, "ms": ms,
                      "ms_iqr": {n: 0.01 for n in names}})

@@ -66,5 +66,9 @@ def test_noalloc_errors():
     with pytest.raises(pa.AttnError) as e:   # output overlaps an input
         pa.attn_fwd_persistent_noalloc(q, q, q, q)
     assert e.value.code == -8
+    with pytest.raises(pa.AttnError) as e:   # paired row blocks: dispatched grid only
+        pa.attn_fwd_persistent_noalloc(q, q, q, torch.empty_like(q),
+                                       mapping=pa.SWIZZLED_HEAD_FIRST | pa.PAIRED)
+    assert e.value.code == -3
     with pytest.raises(ValueError):
         pa.attn_fwd_persistent_noalloc(q, q, q, None)
