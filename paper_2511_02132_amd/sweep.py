@@ -96,7 +96,11 @@ def parse(argv=None):
     p.add_argument("--manifest", default=None)
     p.add_argument("--summarise", action="store_true")
     p.add_argument("--timing", nargs="*", default=[])
-    p.add_argument("--counters", default=None)
+    p.add_argument("--counters", nargs="*", default=[],
+                   help="counter directories of --profile runs, one per --manifests entry")
+    p.add_argument("--manifests", nargs="*", default=[],
+                   help="the manifests of those runs (summary mode; a later run's launch of a "
+                        "configuration replaces an earlier one)")
     p.add_argument("--out", default=None)
     p.add_argument("--cmd", default="")
     p.add_argument("--note", default="", help="extra paragraph for the summary")
@@ -379,8 +383,13 @@ def summarise(a):
                     r = json.loads(x)
                     recs[(r["S"], r["B"], r["Hq"], r["Hkv"])] = r
     recs = [recs[k] for k in sorted(recs)]
-    l2 = l2_by_launch(a.counters, a.manifest) if a.counters else {}
-    l2r = l2_read_bounds_by_launch(a.counters, a.manifest) if a.counters else {}
+    manifests = a.manifests or ([a.manifest] if a.manifest else [])
+    if len(manifests) != len(a.counters):
+        raise SystemExit("--counters and --manifests must pair up")
+    l2, l2r = {}, {}
+    for cdir, man in zip(a.counters, manifests):
+        l2.update(l2_by_launch(cdir, man))
+        l2r.update(l2_read_bounds_by_launch(cdir, man))
     causal = recs[0]["causal"] if recs else True
     which = recs[0].get("pass", "fwd") if recs else "fwd"
     names = [n for n, _ in variants(causal, recs[0].get("d", D) if recs else D, which == "bwd")]

@@ -107,7 +107,7 @@ def test_sweep_summary(tmp_path):
     timing = tmp_path / "t.jsonl"
     timing.write_text("".join(json.dumps(r) + "\n" for r in recs))
     out = tmp_path / "s.md"
-    args = SimpleNamespace(timing=[str(timing)], counters=None, manifest=None, out=str(out),
+    args = SimpleNamespace(timing=[str(timing)], counters=[], manifest=None, manifests=[], out=str(out),
                            cmd="CMD", note="NOTE")
     sweep.summarise(args)
     text = out.read_text()
