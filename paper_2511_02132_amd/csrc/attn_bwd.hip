@@ -82,11 +82,14 @@ __global__ __launch_bounds__(256) void attn_bwd_delta_kernel(const BwdArgs p) {
 
 constexpr int kKeysPerWg = 128;
 constexpr int kQTile = 32;
+// LDS operand reads issued ahead of the MFMA that consumes them, in MFMA steps.
+constexpr int kReadAhead = 1;
 
-// Declared for two waves per SIMD (two workgroups per CU): the compiler then
-// keeps it within 256 registers by spilling three of the K/V operand registers
-// (48 bytes per lane, reloaded once per query tile), and the second workgroup
-// more than hides the reloads.
+// Declared for two waves per SIMD (two workgroups per CU), so a wave has 256
+// registers: the block's K and V operands (64), the dK and dV accumulators
+// (128), S and dP (32) and the operands in flight.  The LDS addresses are
+// rebuilt per tile from three registers instead of sixteen (see compute), which
+// keeps it within 256 without spills.
 template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) {
     constexpr int BQ = kQTile;
@@ -156,11 +159,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
             lds_copy16(buffer_words(p.delta + row0, nrows * 4), lane * 16, dst + 2 * TILE + STAT);
     };
 
-    uint32_t row_off[KSTEPS];   // A operand rows: row c, logical chunk 2kk + h
-#pragma unroll
-    for (int kk = 0; kk < KSTEPS; ++kk) row_off[kk] = sw_off(c, (2 * kk + h) * 16);
-    uint32_t tro[DBLK][2];
-    tr_offsets(lane, tro);
+    // A operand rows of the S and dP products: row c, logical chunk 2kk + h,
+    // at sw_off(c, 32kk + 16h) = rb ^ 32kk (the swizzle flips bits 4-7 only and
+    // rb's bits 5-7 are those of kk = 0).  The transposing reads' offsets are
+    // tro[db][hi] = tb[hi] ^ 64db for the same reason.
+    uint32_t rb = sw_off(c, 16 * h);
+    uint32_t tb[2];
+    {
+        uint32_t tro0[DBLK][2];
+        tr_offsets(lane, tro0);
+        tb[0] = tro0[0][0];
+        tb[1] = tro0[0][1];
+    }
 
     f32x16 dvacc[DBLK], dkacc[DBLK];
 #pragma unroll
@@ -178,14 +188,45 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
         lds_char *const lseb = qb + 2 * TILE;
         lds_char *const db_ = lseb + STAT;
 
-        f32x16 sacc = {}, dpacc = {};
+        // Offsets rebuilt for this tile (one XOR per read) rather than held in
+        // sixteen registers across the loop: the empty asm hides that they
+        // are loop invariant.
+        asm volatile("" : "+v"(rb), "+v"(tb[0]), "+v"(tb[1]));
+        uint32_t row_off[KSTEPS];
 #pragma unroll
-        for (int kk = 0; kk < KSTEPS; ++kk) {
-            const bf16x8 aq = *(const lds_bf16x8 *)(qb + row_off[kk]);
-            sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, kreg[kk], sacc, 0, 0, 0);
-            const bf16x8 ado = *(const lds_bf16x8 *)(dob + row_off[kk]);
-            dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ado, vreg[kk], dpacc, 0, 0, 0);
+        for (int kk = 0; kk < KSTEPS; ++kk) row_off[kk] = rb ^ (uint32_t)(32 * kk);
+        uint32_t tro[DBLK][2];
+#pragma unroll
+        for (int db = 0; db < DBLK; ++db) {
+            tro[db][0] = tb[0] ^ (uint32_t)(64 * db);
+            tro[db][1] = tb[1] ^ (uint32_t)(64 * db);
         }
+
+        // S and dP.  Each step's two A operands are read kReadAhead steps
+        // before its two MFMAs (pinned by the group barriers); left to itself
+        // the compiler waits for every read right before its MFMA.
+        f32x16 sacc = {}, dpacc = {};
+        __builtin_amdgcn_sched_barrier(0);
+        {
+            bf16x8 aq[KSTEPS], ado[KSTEPS];
+#pragma unroll
+            for (int kk = 0; kk < KSTEPS; ++kk) {
+                aq[kk] = *(const lds_bf16x8 *)(qb + row_off[kk]);
+                ado[kk] = *(const lds_bf16x8 *)(dob + row_off[kk]);
+            }
+#pragma unroll
+            for (int kk = 0; kk < KSTEPS; ++kk) {
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[kk], kreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ado[kk], vreg[kk], dpacc, 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * kReadAhead, 0);
+#pragma unroll
+            for (int kk = 0; kk < KSTEPS; ++kk) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+                if (kk + kReadAhead < KSTEPS) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
         // Register r holds query row 8(r/4) + 4h + r%4 of the tile.
         const bool need_mask = CAUSAL && q0 < kw0 + 31;
         f32x8 p8[2], ds8[2];
@@ -208,16 +249,36 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
             pb[kc] = __builtin_convertvector(p8[kc], bf16x8);
             dsb[kc] = __builtin_convertvector(ds8[kc], bf16x8);
         }
+        // dV and dK, each MFMA's transposed operand (two reads) read
+        // kReadAhead MFMAs ahead.
+        constexpr int NPROD = 2 * 2 * DBLK;
+        __builtin_amdgcn_sched_barrier(0);
+        {
+            bf16x8 av[2][DBLK], ak[2][DBLK];
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
+            for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-            for (int db = 0; db < DBLK; ++db) {
-                dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(dob, tro, db, kc),
-                                                                     pb[kc], dvacc[db], 0, 0, 0);
-                dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(qb, tro, db, kc),
-                                                                     dsb[kc], dkacc[db], 0, 0, 0);
+                for (int db = 0; db < DBLK; ++db) {
+                    av[kc][db] = tr_operand(dob, tro, db, kc);
+                    ak[kc][db] = tr_operand(qb, tro, db, kc);
+                }
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                for (int db = 0; db < DBLK; ++db) {
+                    dvacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[kc][db], pb[kc], dvacc[db],
+                                                                         0, 0, 0);
+                    dkacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[kc][db], dsb[kc], dkacc[db],
+                                                                         0, 0, 0);
+                }
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * kReadAhead, 0);
+#pragma unroll
+            for (int i = 0; i < NPROD; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                if (i + kReadAhead < NPROD) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
             }
         }
+        __builtin_amdgcn_sched_barrier(0);
     };
 
     if (total > 0) copy_tile(0, 0);
@@ -239,8 +300,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
         (void *)((char *)p.dk + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
     const __amdgpu_buffer_rsrc_t rdv = __builtin_amdgcn_make_buffer_rsrc(
         (void *)((char *)p.dv + kv_head * 2), 0, p.Skv * ROW_BYTES, kBufferFlags);
-    store_rows(dkacc, p.scale, rdk, my_key, h);
-    store_rows(dvacc, 1.0f, rdv, my_key, h);
+    // Without the causal mask the loop does not use the lane's key: rebuilt
+    // here instead of held in a register across the loop.
+    const int key_e = CAUSAL ? my_key : kw0 + (lane_index_here() & 31);
+    store_rows(dkacc, p.scale, rdk, key_e, h);
+    store_rows(dvacc, 1.0f, rdv, key_e, h);
 }
 
 // ---------------------------------------------------------------- launchers

@@ -20,6 +20,19 @@ constexpr int KSTEPS = D / 16;   // MFMA k-steps over the head dimension
 constexpr int DBLK = D / 32;     // 32-row blocks of a transposed gradient
 constexpr float kLog2e = 1.44269504088896340736f;
 
+// The calling lane's index, computed where it is called: the volatile asm is
+// neither hoisted nor merged with an earlier copy, so no register has to hold
+// the lane index across a loop.
+__device__ __forceinline__ int lane_index_here() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+}
+
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
+
 // Chunk c (16 bytes) of row r of a tile is stored at c ^ dual_swizzle(r).
 //  * 16-byte row reads: 16 consecutive rows, one logical chunk -> the 16
 //    values of dual_swizzle over 16 consecutive rows are all distinct.
