@@ -28,6 +28,9 @@ ARCH = "gfx950"
 # The forward kernels and the headers they include: the counter summaries
 # under profiles/ describe these, so their hash ties a summary to its code.
 KERNEL_SOURCES = ["attn_fwd.hip", "attn_fwd_pp.hip", "attn_device.h", "attn_internal.h"]
+# The backward kernels and their headers, for the backward's summaries.
+BWD_KERNEL_SOURCES = ["attn_bwd.hip", "attn_bwd_dq.hip", "attn_bwd_common.h", "attn_device.h",
+                      "attn_internal.h"]
 
 
 def code_tokens(text: str) -> str:
@@ -57,13 +60,14 @@ def code_tokens(text: str) -> str:
     return " ".join("".join(out).split())
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(names=None) -> str:
     """Short hash of the kernel sources (comments and layout ignored): ties a
-    counter summary to the code it measured."""
+    counter summary to the code it measured.  names: the files hashed (default:
+    the forward kernels)."""
     import hashlib
 
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in (names or KERNEL_SOURCES):
         with open(os.path.join(CSRC, name)) as f:
             h.update(code_tokens(f.read()).encode())
     return h.hexdigest()[:16]

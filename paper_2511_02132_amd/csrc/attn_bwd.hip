@@ -228,7 +228,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
         }
         __builtin_amdgcn_sched_barrier(0);
         // Register r holds query row 8(r/4) + 4h + r%4 of the tile.
-        const bool need_mask = CAUSAL && q0 < kw0 + 31;
+        // Row 8j + 4h + e of the tile sees the lane's key iff 8j + e >= first_row
+        // (no row is masked when first_row <= 0, e.g. without a causal mask).
+        const int first_row = CAUSAL ? my_key - q0 - 4 * h : 0;
         f32x8 p8[2], ds8[2];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -238,7 +240,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
             for (int e = 0; e < 4; ++e) {
                 const int r = 4 * j + e;
                 float pr = exp2_hw(__builtin_fmaf(sacc[r], sl2, -l4[e] * kLog2e));
-                if (need_mask && my_key > q0 + 8 * j + 4 * h + e) pr = 0.0f;
+                if (CAUSAL && 8 * j + e < first_row) pr = 0.0f;
                 p8[r >> 3][r & 7] = pr;
                 ds8[r >> 3][r & 7] = pr * (dpacc[r] - d4[e]);
             }

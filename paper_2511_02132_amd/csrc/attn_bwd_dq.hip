@@ -128,16 +128,17 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(const BwdArgs p) {
             }
         }
         // Register r of block kb2 holds key 32kb2 + 8(r/4) + 4h + r%4 of the tile.
+        // Key 32kb2 + 8(r/4) + 4h + r%4 of the tile is seen by the lane's row
+        // iff 32kb2 + 8(r/4) + r%4 <= last_key (always, without a causal mask).
         const int key0 = n * BN;
-        const bool need_mask = CAUSAL && key0 + BN - 1 > q_wave0;
+        const int last_key = CAUSAL ? my_q - key0 - 4 * h : BN;
         f32x8 ds8[4];
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 float pr = exp2_hw(__builtin_fmaf(sacc[kb2][r], sl2, -lse2));
-                const int key = key0 + 32 * kb2 + 8 * (r >> 2) + 4 * h + (r & 3);
-                if (need_mask && key > my_q) pr = 0.0f;
+                if (CAUSAL && 32 * kb2 + 8 * (r >> 2) + (r & 3) > last_key) pr = 0.0f;
                 ds8[2 * kb2 + (r >> 3)][r & 7] = pr * (dpacc[kb2][r] - dq_d);
             }
         bf16x8 dsb[4];

@@ -95,7 +95,7 @@ def summarise_kernels(dirs):
 def write_kernels_md(out: str, title: str, cmd: str, dirs, note: str = ""):
     """Per-kernel counter table (MFMA utilisation, LDS instructions per MFMA,
     LDS waits, L2 hits, HBM bytes) of the passes in dirs."""
-    from paper_2511_02132_amd.build import kernel_source_hash
+    from paper_2511_02132_amd.build import BWD_KERNEL_SOURCES, kernel_source_hash
 
     res, fac = summarise_kernels(dirs)
     lines = ["# %s" % title, "", "Commands (run from the repository root; `cd /tmp` first, "
@@ -106,7 +106,8 @@ def write_kernels_md(out: str, title: str, cmd: str, dirs, note: str = ""):
     if fac:
         lines.append("Copy-kernel scale factors (256 MiB device copy): %s." % ", ".join(
             "%s x%.4f" % (c, f) for c, f in sorted(fac.items())))
-    lines += ["Kernel source sha256[:16] (forward kernels): `%s`" % kernel_source_hash(), "",
+    lines += ["Kernel source sha256[:16]: forward kernels `%s`, backward kernels `%s`" % (
+                  kernel_source_hash(), kernel_source_hash(BWD_KERNEL_SOURCES)), "",
               "| kernel | MFMA util % | MFMA instr | LDS instr | LDS / MFMA | LDS wait / LDS instr "
               "| VALU instr | L2 hit | HBM bytes read | HBM bytes written |",
               "|---|---|---|---|---|---|---|---|---|---|"]
@@ -129,7 +130,9 @@ def write_kernels_md(out: str, title: str, cmd: str, dirs, note: str = ""):
             f(100.0 * hit / (hit + miss) if hit is not None and miss is not None and hit + miss > 0
               else None, "%.1f%%"),
             f(rd, "%.3e"), f(wr, "%.3e")))
-    data = {"kernel_source_sha256": kernel_source_hash(), "scale": fac, "per_kernel": res}
+    data = {"kernel_source_sha256": kernel_source_hash(),
+            "bwd_kernel_source_sha256": kernel_source_hash(BWD_KERNEL_SOURCES), "scale": fac,
+            "per_kernel": res}
     lines += ["", "```json", json.dumps(data, indent=1, sort_keys=True), "```", ""]
     with open(out, "w") as fh:
         fh.write("\n".join(lines))
@@ -357,6 +360,52 @@ def write_stats_md(out: str, stats_csv: str, bench_json: str, cmd: str):
         f.write("\n".join(lines))
 
 
+def write_bwd_stats_md(out: str, title: str, stats_csv: str, cmd: str, shape, note: str = ""):
+    """Kernel-trace statistics of the backward's kernels (D, dK/dV and dQ per
+    variant) and the headline variant's total.  shape: (B, Hq, S) of the run,
+    causal, head dimension 128."""
+    import paper_2511_02132_amd as pa
+    from paper_2511_02132_amd.build import BWD_KERNEL_SOURCES, kernel_source_hash
+
+    rows = []
+    for r in csv.DictReader(open(stats_csv)):
+        k = kernel_of(r["Name"])
+        if k is None or not (k == "D" or k.startswith("dK/dV ") or k.startswith("dQ ")):
+            continue
+        rows.append((k, int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+                     float(r["MaxNs"]) / 1e3))
+    order = {"D": 0, "dK/dV": 1, "dQ": 2}
+    rows.sort(key=lambda x: (order[x[0].split(" ")[0]], x[2]))
+    lines = ["# %s" % title, "", "Command (run from the repository root; `cd /tmp` first, "
+             "paths absolute in the run):", "", "```", cmd.strip(), "```", ""]
+    if note:
+        lines += [note, ""]
+    lines += ["Backward kernel source sha256[:16]: `%s`" % kernel_source_hash(BWD_KERNEL_SOURCES),
+              "", "| kernel | calls | average us | min us | max us |", "|---|---|---|---|---|"]
+    for k, n, avg, mn, mx in rows:
+        lines.append("| %s | %d | %.1f | %.1f | %.1f |" % (k, n, avg, mn, mx))
+    head = pa.method_variant(True)
+    dq_name = "dQ " + pa.variant_name(head)
+    # the dK/dV kernel takes only the block-major bit of the order
+    dkdv_name = "dK/dV " + pa.variant_name(head & ~pa.HEAVY_FIRST)
+    avg = {k: a for k, _, a, _, _ in rows}
+    if all(x in avg for x in ("D", dkdv_name, dq_name)):
+        B, Hq, S = shape
+        total = avg["D"] + avg[dkdv_name] + avg[dq_name]
+        fl = 2.5 * pa.attention_flops(B, Hq, S, S, 128, True)
+        lines += ["", "Headline variant `%s` (the dK/dV kernel takes only the block-major bit "
+                  "of the order: its natural order already starts with the heaviest causal key "
+                  "block): D %.1f + dK/dV %.1f + dQ %.1f = %.1f us, %.0f TFLOP/s in the "
+                  "FlashAttention convention (2.5x the forward flops); the dK/dV kernel, counting "
+                  "its four products (twice the forward flops), runs at %.0f TFLOP/s." % (
+                      pa.variant_name(head), avg["D"], avg[dkdv_name], avg[dq_name], total,
+                      fl / total / 1e6,
+                      2.0 * pa.attention_flops(B, Hq, S, S, 128, True) / avg[dkdv_name] / 1e6)]
+    lines.append("")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+
+
 def main(argv=None):
     p = argparse.ArgumentParser()
     p.add_argument("--workload")
@@ -368,9 +417,15 @@ def main(argv=None):
                    help="write a per-kernel counter table (any attention kernels, the "
                         "backward's included) with this title")
     p.add_argument("--note", default="")
+    p.add_argument("--bwd-trace", metavar="TITLE",
+                   help="with --stats-csv: a backward kernel-trace table with this title")
+    p.add_argument("--shape", type=int, nargs=3, metavar=("B", "HQ", "S"),
+                   help="the backward run's shape (causal, d = 128)")
     p.add_argument("dirs", nargs="*")
     a = p.parse_args(argv)
-    if a.per_kernel:
+    if a.bwd_trace:
+        write_bwd_stats_md(a.out, a.bwd_trace, a.stats_csv, a.cmd, a.shape, a.note)
+    elif a.per_kernel:
         write_kernels_md(a.out, a.per_kernel, a.cmd, a.dirs, a.note)
     elif a.stats_csv:
         write_stats_md(a.out, a.stats_csv, a.bench_json, a.cmd)

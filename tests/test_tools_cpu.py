@@ -286,3 +286,30 @@ def test_per_kernel_counter_table(tmp_path):
     rc.write_kernels_md(str(out), "T", "CMD", [str(d)])
     line = [l for l in out.read_text().splitlines() if l.startswith("| dQ ")][0]
     assert "| 1.50 |" in line and "2.048e+04" in line
+
+
+def test_backward_trace_summary(tmp_path):
+    """The backward kernel-trace table lists D, dK/dV and dQ per variant and adds
+    up the headline variant's three kernels (the dK/dV kernel carries only the
+    block-major bit of the order) into FlashAttention-convention TFLOP/s."""
+    ns = "void attn::(anonymous namespace)::"
+    stats = tmp_path / "stats.csv"
+    rows = [("attn::(anonymous namespace)::attn_bwd_delta_kernel(attn::BwdArgs)", 9, 40000.0),
+            (ns + "attn_bwd_dkdv_kernel<true, 2, 0>(attn::BwdArgs)", 2, 1000000.0),
+            (ns + "attn_bwd_dkdv_kernel<true, 0, 0>(attn::BwdArgs)", 2, 1200000.0),
+            (ns + "attn_bwd_dq_kernel<true, 2, 1>(attn::BwdArgs)", 1, 500000.0),
+            (ns + "attn_fwd_pp_kernel<true, 2, 1>(attn::KernelArgs)", 9, 300000.0)]
+    with open(stats, "w") as f:
+        f.write('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs"\n')
+        for name, calls, avg in rows:
+            f.write('"%s",%d,%d,%f,1.0,%d,%d\n' % (name, calls, calls * avg, avg, avg, avg))
+    out = tmp_path / "t.md"
+    rc.write_bwd_stats_md(str(out), "T", str(stats), "CMD", (1, 32, 8192))
+    text = out.read_text()
+    body = [l for l in text.splitlines() if l.startswith("| ") and "---" not in l][1:]
+    assert [l.split("|")[1].strip() for l in body] == [
+        "D", "dK/dV swizzled_head_first", "dK/dV naive_block_first",
+        "dQ swizzled_head_first+heavy_first"]
+    fl = 2.5 * pa.attention_flops(1, 32, 8192, 8192, 128, True)
+    assert "D 40.0 + dK/dV 1000.0 + dQ 500.0 = 1540.0 us" in text
+    assert "%.0f TFLOP/s in the" % (fl / 1540.0 / 1e6) in text
