@@ -160,9 +160,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
     };
 
     // A operand rows of the S and dP products: row c, logical chunk 2kk + h,
-    // at sw_off(c, 32kk + 16h) = rb ^ 32kk (the swizzle flips bits 4-7 only and
-    // rb's bits 5-7 are those of kk = 0).  The transposing reads' offsets are
-    // tro[db][hi] = tb[hi] ^ 64db for the same reason.
+    // at sw_off(c, 32kk + 16h) = rb ^ 32kk, since the chunk index reaches the
+    // offset (bits 4-7) only through an XOR with the row's swizzle.  For the
+    // same reason the transposing reads' offsets are tro[db][hi] = tb[hi] ^ 64db.
     uint32_t rb = sw_off(c, 16 * h);
     uint32_t tb[2];
     {
