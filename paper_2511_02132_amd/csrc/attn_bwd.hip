@@ -188,19 +188,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
         lds_char *const lseb = qb + 2 * TILE;
         lds_char *const db_ = lseb + STAT;
 
-        // Offsets rebuilt for this tile (one XOR per read) rather than held in
-        // sixteen registers across the loop: the empty asm hides that they
-        // are loop invariant.
-        asm volatile("" : "+v"(rb), "+v"(tb[0]), "+v"(tb[1]));
+        // Offsets rebuilt for this tile (one XOR per read), each set right
+        // before the step that uses it, rather than held in sixteen registers
+        // across the loop: the empty asm hides that they are loop invariant.
+        asm volatile("" : "+v"(rb));
         uint32_t row_off[KSTEPS];
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) row_off[kk] = rb ^ (uint32_t)(32 * kk);
-        uint32_t tro[DBLK][2];
-#pragma unroll
-        for (int db = 0; db < DBLK; ++db) {
-            tro[db][0] = tb[0] ^ (uint32_t)(64 * db);
-            tro[db][1] = tb[1] ^ (uint32_t)(64 * db);
-        }
 
         // S and dP.  Each step's two A operands are read kReadAhead steps
         // before its two MFMAs (pinned by the group barriers); left to itself
@@ -227,33 +221,55 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
             }
         }
         __builtin_amdgcn_sched_barrier(0);
-        // Register r holds query row 8(r/4) + 4h + r%4 of the tile.
-        // Row 8j + 4h + e of the tile sees the lane's key iff 8j + e >= first_row
-        // (no row is masked when first_row <= 0, e.g. without a causal mask).
+        // Register r holds query row 8(r/4) + 4h + r%4 of the tile, so
+        // registers 8kc..8kc+7 are rows 16kc..16kc+15: the k-block kc of the
+        // dV and dK products.  Row 8j + 4h + e of the tile sees the lane's key
+        // iff 8j + e >= first_row (no row is masked when first_row <= 0, e.g.
+        // without a causal mask).
         const int first_row = CAUSAL ? my_key - q0 - 4 * h : 0;
-        f32x8 p8[2], ds8[2];
+        f32x4 lse4[4], d4[4];   // statistics of rows 8j + 4h .. +3
+        auto read_stats = [&](const int kc) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const f32x4 l4 = *(const lds_f32x4 *)(lseb + (8 * j + 4 * h) * 4);
-            const f32x4 d4 = *(const lds_f32x4 *)(db_ + (8 * j + 4 * h) * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 4 * j + e;
-                float pr = exp2_hw(__builtin_fmaf(sacc[r], sl2, -l4[e] * kLog2e));
-                if (CAUSAL && 8 * j + e < first_row) pr = 0.0f;
-                p8[r >> 3][r & 7] = pr;
-                ds8[r >> 3][r & 7] = pr * (dpacc[r] - d4[e]);
+            for (int j = 2 * kc; j < 2 * kc + 2; ++j) {
+                lse4[j] = *(const lds_f32x4 *)(lseb + (8 * j + 4 * h) * 4);
+                d4[j] = *(const lds_f32x4 *)(db_ + (8 * j + 4 * h) * 4);
             }
-        }
+        };
+        // P and dS of k-block kc, as bf16 B operands
         bf16x8 pb[2], dsb[2];
+        auto softmax_block = [&](auto kc_c) __attribute__((always_inline)) {
+            constexpr int KC = decltype(kc_c)::value;
+            f32x8 p8, ds8;
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-            pb[kc] = __builtin_convertvector(p8[kc], bf16x8);
-            dsb[kc] = __builtin_convertvector(ds8[kc], bf16x8);
-        }
+            for (int j = 2 * KC; j < 2 * KC + 2; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = 4 * j + e;
+                    float pr = exp2_hw(__builtin_fmaf(sacc[r], sl2, -lse4[j][e] * kLog2e));
+                    if (CAUSAL && 8 * j + e < first_row) pr = 0.0f;
+                    p8[r & 7] = pr;
+                    ds8[r & 7] = pr * (dpacc[r] - d4[j][e]);
+                }
+            pb[KC] = __builtin_convertvector(p8, bf16x8);
+            dsb[KC] = __builtin_convertvector(ds8, bf16x8);
+        };
+        // k-block 0 now; k-block 1's statistics are read here and its softmax
+        // runs between the k-block 0 MFMAs below.
+        read_stats(0);
+        softmax_block(Int<0>{});
+        __builtin_amdgcn_sched_barrier(0);
+        read_stats(1);
         // dV and dK, each MFMA's transposed operand (two reads) read
-        // kReadAhead MFMAs ahead.
+        // kReadAhead MFMAs ahead, and k-block 1's softmax spread over the
+        // k-block 0 MFMAs, which need only k-block 0's P and dS.
         constexpr int NPROD = 2 * 2 * DBLK;
+        asm volatile("" : "+v"(tb[0]), "+v"(tb[1]));
+        uint32_t tro[DBLK][2];
+#pragma unroll
+        for (int db = 0; db < DBLK; ++db) {
+            tro[db][0] = tb[0] ^ (uint32_t)(64 * db);
+            tro[db][1] = tb[1] ^ (uint32_t)(64 * db);
+        }
         __builtin_amdgcn_sched_barrier(0);
         {
             bf16x8 av[2][DBLK], ak[2][DBLK];
@@ -264,6 +280,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
                     av[kc][db] = tr_operand(dob, tro, db, kc);
                     ak[kc][db] = tr_operand(qb, tro, db, kc);
                 }
+            softmax_block(Int<1>{});
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
@@ -278,6 +295,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) 
             for (int i = 0; i < NPROD; ++i) {
                 __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
                 if (i + kReadAhead < NPROD) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+                if (i < NPROD / 2) {
+                    __builtin_amdgcn_sched_group_barrier(kSchedValu, 8, 0);
+                    __builtin_amdgcn_sched_group_barrier(kSchedTrans, 1, 0);
+                }
             }
         }
         __builtin_amdgcn_sched_barrier(0);

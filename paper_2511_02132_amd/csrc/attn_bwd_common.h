@@ -30,8 +30,10 @@ __device__ __forceinline__ int lane_index_here() {
 }
 
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedValu = 0x002;   // vector ALU, transcendentals excluded
 constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
+constexpr int kSchedTrans = 0x400;
 
 // Chunk c (16 bytes) of row r of a tile is stored at c ^ dual_swizzle(r).
 //  * 16-byte row reads: 16 consecutive rows, one logical chunk -> the 16
