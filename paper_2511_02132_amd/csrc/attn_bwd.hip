@@ -90,6 +90,9 @@ constexpr int kReadAhead = 1;
 // (128), S and dP (32) and the operands in flight.  The LDS addresses are
 // rebuilt per tile from three registers instead of sixteen (see compute), which
 // keeps it within 256 without spills.
+// Per query tile a wave computes S and dP, then P and dS of the tile's first 16
+// rows, then the dV and dK MFMAs of those rows with the softmax of the other 16
+// rows issued between them, then the MFMAs of the other rows.
 template <bool CAUSAL, int MAPPING, int ORDER>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(const BwdArgs p) {
     constexpr int BQ = kQTile;
