@@ -157,6 +157,43 @@ def test_backward_full_size_sampled_rows():
         assert torch.isfinite(t.float()).all()
 
 
+def test_backward_gqa_noncausal_ragged_sampled():
+    """GQA (groups of four), no mask, 4000 rows and keys (ragged 128-key and 64-key
+    blocks): sampled dQ rows and dK/dV keys vs the oracle."""
+    B, Hq, Hkv, S, causal = 1, 16, 4, 4000, False
+    _say("bwd gqa non-causal ragged", B, Hq, Hkv, S)
+    q, k, v, do = _inputs(B, Hq, Hkv, S, S, 7400)
+    qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
+    scale = ai.default_scale(D)
+    _, _, dq, dk, dv = _grads(qd, kd, vd, dod, causal, scale, mapping=pa.SWIZZLED_HEAD_FIRST | 0x10)
+    qb, kb, vb, dob = (ai.bf16_bits(t) for t in (q, k, v, do))
+    rng = np.random.default_rng(6)
+    rows = np.array([[0, h, i] for h in (0, 13)
+                     for i in [0, 31, 32, 3967, 3968, 3999] + list(rng.integers(0, S, 8))], np.int64)
+    rq = oracle.attn_bwd_dq_rows_f64(qb, kb, vb, dob, rows, causal, scale)
+    got = dq.float().cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
+    _check("dq rows", torch.from_numpy(got), rq)
+    # dK/dV of K/V head 1 sum over query heads 4-7: their statistics for every row
+    g = 1
+    heads = range(4 * g, 4 * g + 4)
+    lse_all = np.zeros((B, Hq, S))
+    D_all = np.zeros((B, Hq, S))
+    for h in heads:
+        hrows = oracle.all_rows(1, 1, S)
+        hrows[:, 1] = h
+        lse_all[0, h], D_all[0, h] = oracle.attn_row_stats_f64(qb, kb, vb, dob, hrows, causal, scale)
+    keys = np.array([[0, g, j] for j in [0, 127, 128, 3967, 3968, 3999] + list(rng.integers(0, S, 6))],
+                    np.int64)
+    rk, rv = oracle.attn_bwd_dkdv_rows_f64(qb, kb, vb, dob, keys, causal, scale,
+                                           stats=(lse_all, D_all))
+    gk = dk.float().cpu().numpy()[keys[:, 0], keys[:, 1], keys[:, 2]]
+    gv = dv.float().cpu().numpy()[keys[:, 0], keys[:, 1], keys[:, 2]]
+    _check("dk rows", torch.from_numpy(gk), rk)
+    _check("dv rows", torch.from_numpy(gv), rv)
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t.float()).all()
+
+
 def test_backward_errors():
     q, k, v, do = (t.to(DEV) for t in _inputs(1, 2, 2, 64, 64, 7300))
     o, lse = pa.attn_fwd_lse(q, k, v, causal=True)
